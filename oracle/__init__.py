@@ -1,0 +1,29 @@
+"""CPU oracle for Traversal Verification (arXiv 2505.12398).
+
+TEST INFRASTRUCTURE ONLY. This package is the plain, slow, fp64 reference that
+the HIP library is checked against. Only ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py`` may import or call anything here;
+the library ``paper_2505_12398_amd`` and its kernels never do, and this package
+imports nothing from them.
+
+Contents:
+
+* :mod:`oracle.tv_oracle` -- Algorithm 3 (Traversal Verification) and the
+  top-down token-level verification (Algorithm 2 applied node by node, Sec. 2.2),
+  written step by step with explicit V-vectors in float64.
+* :mod:`oracle.enumerate` -- exact output laws by enumerating every draft tree
+  and every accept/reject branch (checks the losslessness theorem, Sec. 3.3).
+
+Pins (what the oracle is checked against, independent of itself) live in
+``tests/test_oracle_*.py`` and ``tests/golden/``. Every function here is pinned;
+none is "parity unpinned".
+"""
+
+from .tv_oracle import (  # noqa: F401
+    WITHOUT_REPLACEMENT, WITH_REPLACEMENT,
+    TREE_OK, TREE_BAD_PARENT, TREE_BAD_TOKEN, TREE_DUP_SIBLING,
+    TREE_NONFINITE, TREE_DEGENERATE,
+    NODE_UNTESTED, NODE_ACCEPTED, NODE_REJECTED, NODE_PRUNED,
+    TreeResult, to_f64, tempered_softmax, inverse_cdf,
+    verify_tree, verify_tree_tokenlevel, algorithmic_bytes,
+)

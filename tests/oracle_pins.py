@@ -1,0 +1,331 @@
+"""Pins for the CPU oracle: checks against what the paper and the mathematics
+fix, never against the oracle itself. Each pin raises AssertionError when
+violated. tests/test_oracle_pins.py runs them on the oracle as written;
+tests/test_oracle_mutations.py plants plausible mistakes in the oracle and
+checks that some pin fails.
+
+All calls go through module attributes (``O.verify_tree``) so that a planted
+mistake in one step is seen by every pin.
+"""
+
+from __future__ import annotations
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+
+import oracle.tv_oracle as O
+import oracle.enumerate as E
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+ALMOST_ONE = np.float32(1.0 - 2.0 ** -24)     # rejects any theta < 1
+
+
+def golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def frac(v):
+    return float(Fraction(v[0], v[1]))
+
+
+def _close(a, b, tol=1e-12, what=""):
+    assert abs(float(a) - float(b)) <= tol, f"{what}: {a!r} != {b!r}"
+
+
+def _single_node_rows(target, draft, n1):
+    zb = np.tile(np.log(np.asarray(target, dtype=np.float64)), (n1, 1))
+    zs = np.tile(np.log(np.asarray(draft, dtype=np.float64)), (n1, 1))
+    return zb, zs
+
+
+# ---------------------------------------------------------------------------
+# Values the paper prints
+# ---------------------------------------------------------------------------
+
+def pin_worked_example_trace():
+    """Sec. 3.2: traversal order, chain rates and the parent update numbers,
+    following every rejection (all uniforms just below 1)."""
+    g = golden("worked_example.json")
+    par, tok, zb, zs, T = W.worked_example()
+    u = np.full(6, ALMOST_ONE, np.float32)
+    u[0] = 0.5
+    r = O.verify_tree(par, tok, zb, zs, T, u, O.WITHOUT_REPLACEMENT)
+    assert r.status == O.TREE_OK
+    assert r.test_order == g["traversal_order"], r.test_order
+    pr = g["printed"]
+    tol = g["printed_tolerance"]
+    _close(r.node_theta[3], pr["accept_chain_X1X3_traversal"], tol, "theta X3 printed")
+    # theta(X4) = p'(X1) * b'(c)/s'(c) with b' = [0,0,1] and s'(c) = 1/7 (Eq. e1, e2)
+    _close(r.node_theta[4] / 7.0, pr["p_prime_X1_after_X3"], tol, "p' X1 printed")
+    _close(r.node_theta[4], pr["accept_chain_X1X4"], tol, "theta X4 printed")
+    _close(r.node_theta[1], pr["p_prime_X1_after_X4"], 0.0, "p' X1 -> 0")
+    ex = g["exact_readings"]
+    for node, key in [(1, "p_ini_X1"), (3, "p_ini_X3")]:
+        _close(r.p_init[node], frac(ex[key]), 1e-12, key)
+    for node, key in [(3, "theta_X3"), (4, "theta_X4"), (1, "theta_X1"), (5, "theta_X5"),
+                      (2, "theta_X2")]:
+        _close(r.node_theta[node], frac(ex[key]), 1e-12, key)
+    assert r.accepted_node == 2 and r.accept_len == 1
+    # Y comes from X2's residual after X5 (token a) is rejected: [0, 1/3, 2/3].
+    _close(r.y_weights[0], 0.0, 0.0, "residual a")
+    _close(r.y_weights[1], 1 / 3, 1e-12, "residual b")
+
+
+def pin_worked_example_tokenlevel():
+    """Sec. 3.2: token-level acceptance of chain X1X3 is 0.5 (X1 at 1/2, X3 sure)."""
+    g = golden("worked_example.json")
+    par, tok, zb, zs, T = W.worked_example()
+    law = {}
+    for w, res in E.decision_branches(
+            lambda d: O.verify_tree_tokenlevel(par, tok, zb, zs, T, None,
+                                               O.WITHOUT_REPLACEMENT, decide=d)):
+        law[res.accepted_node] = law.get(res.accepted_node, 0.0) + w
+    _close(law.get(3, 0.0), g["printed"]["accept_chain_X1X3_tokenlevel"], 1e-12, "TL X1X3")
+
+
+def pin_worked_example_law():
+    """Exact accept law of both verifiers on the Sec. 3.2 tree (products of the
+    printed steps)."""
+    g = golden("worked_example.json")["derived_law"]
+    par, tok, zb, zs, T = W.worked_example()
+    for ver, key, tkey in [(O.verify_tree, "traversal_accepted_node", "traversal_expected_tau"),
+                           (O.verify_tree_tokenlevel, "tokenlevel_accepted_node",
+                            "tokenlevel_expected_tau")]:
+        law = {}
+        etau = 0.0
+        for w, res in E.decision_branches(
+                lambda d: ver(par, tok, zb, zs, T, None, O.WITHOUT_REPLACEMENT, decide=d)):
+            law[res.accepted_node] = law.get(res.accepted_node, 0.0) + w
+            etau += w * res.accept_len
+        want = {int(k): frac(v) for k, v in g[key].items()}
+        assert set(law) == set(want), (key, law)
+        for k, v in want.items():
+            _close(law[k], v, 1e-12, f"{key}[{k}]")
+        _close(etau, frac(g[tkey]), 1e-12, tkey)
+
+
+def pin_single_token_table1():
+    """Sec. 2.1 Table 1: acceptance probability of each drafted token, the
+    residual after rejecting a, and an output law equal to the target."""
+    g = golden("single_token.json")
+    par = np.array([-1, 0], np.int32)
+    zb, zs = _single_node_rows(g["target"], g["draft"], 2)
+    resid = np.asarray(g["residual_unnormalised"], dtype=np.float64)
+    np.testing.assert_allclose(resid / resid.sum(), [frac(v) for v in g["residual"]],
+                               atol=1e-12)
+    first = np.zeros(3)
+    for x, name in enumerate("abc"):
+        tok = np.array([0, x], np.int32)
+        acc = 0.0
+        for w, res in E.decision_branches(
+                lambda d: O.verify_tree(par, tok, zb, zs, 1.0, None, O.WITHOUT_REPLACEMENT,
+                                        decide=d)):
+            if res.accepted_node == 1:
+                acc += w
+            else:   # rejected: Y from the normalised residual [M_b - M_s]_+
+                assert res.accepted_node == 0
+                np.testing.assert_allclose(res.y_weights, resid / resid.sum(), atol=1e-12)
+        _close(acc, g["accept_prob"][name], 1e-12, f"accept {name}")
+        law = E.fixed_tree_law(O.verify_tree, par, tok, zb, zs, 1.0, O.WITHOUT_REPLACEMENT)
+        for seq, p in law.items():
+            first[seq[0]] += g["draft"][x] * p
+    # Drafting x with M_s(x) and verifying: the first output token follows M_b.
+    np.testing.assert_allclose(first, g["target"], atol=1e-12)
+
+
+def pin_rrsw_example():
+    """Sec. 2.2: after rejecting a, residual [0,1/3,2/3], draft [0,3/4,1/4], and a
+    second candidate b is accepted with probability 4/9 (c with certainty).
+    A root with two leaf children: both verifiers coincide here."""
+    g = golden("rrsw_example.json")
+    par = np.array([-1, 0, 0], np.int32)
+    zb, zs = _single_node_rows(g["target"], g["draft"], 3)
+    for second, key in [(1, "b"), (2, "c")]:
+        tok = np.array([0, 0, second], np.int32)
+        u = np.array([0.5, ALMOST_ONE, 0.5], np.float32)
+        for ver in (O.verify_tree, O.verify_tree_tokenlevel):
+            r = ver(par, tok, zb, zs, 1.0, u, O.WITHOUT_REPLACEMENT)
+            _close(r.node_theta[1], 0.5, 1e-12, "first candidate")
+            _close(r.node_theta[2], frac(g["accept_prob_second_candidate"][key]), 1e-12,
+                   f"second candidate {key}")
+    # Residual after rejecting both a and b: Y's distribution at the root.
+    tok = np.array([0, 0, 1], np.int32)
+    u = np.array([0.5, ALMOST_ONE, ALMOST_ONE], np.float32)
+    r = O.verify_tree_tokenlevel(par, tok, zb, zs, 1.0, u, O.WITHOUT_REPLACEMENT)
+    res_a = np.array([frac(v) for v in g["after_rejecting_a"]["residual_target"]])
+    drf_a = np.array([frac(v) for v in g["after_rejecting_a"]["draft_without_a"]])
+    want = np.maximum(res_a - drf_a, 0)
+    np.testing.assert_allclose(r.y_weights, want / want.sum(), atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Mathematics the paper fixes
+# ---------------------------------------------------------------------------
+
+def pin_tempered_softmax_inverse():
+    """softmax(T * log p / T) = p for any T > 0 (temperature undoes its own
+    scaling), and the largest logit keeps the largest probability."""
+    rng = np.random.default_rng(7)
+    p = rng.dirichlet(np.ones(11))
+    for T in (0.7, 1.0, 1.9):
+        q = O.tempered_softmax(T * np.log(p), np.float32(T))
+        np.testing.assert_allclose(q, p, rtol=1e-6, atol=1e-12)
+    z = rng.normal(size=9)
+    a = O.tempered_softmax(z, np.float32(0.5))
+    b = O.tempered_softmax(z, np.float32(2.0))
+    assert a.max() > b.max()    # lower temperature sharpens
+
+
+def pin_inverse_cdf_law():
+    """The final sample has law w / sum(w): over the 2^12 grid of uniforms
+    u = k / 2^12 each token's count is its weight times 2^12 up to one."""
+    w = np.array([0.0, 3.0, 1.0, 0.0, 4.0, 0.5, 0.0, 7.5])
+    n = 2 ** 12
+    counts = np.zeros(len(w))
+    for k in range(n):
+        y, _ = O.inverse_cdf(w, k / n)
+        counts[y] += 1
+    want = w / w.sum() * n
+    assert np.all(np.abs(counts - want) <= 1.0), (counts, want)
+    assert counts[w == 0].sum() == 0
+
+
+def pin_lossless_exact():
+    """Theorem thm:TV_valid via Lemma l1: the padded output law equals the
+    target law, over all draft trees of a tiny context model, in both matched
+    sibling modes, for Traversal Verification and the token-level baseline."""
+    m = W.ContextModel(3, seed=0)
+    par = W.binary_parents(2)
+    tl = E.target_law(m, 1.0, 3)
+    for ver in (O.verify_tree, O.verify_tree_tokenlevel):
+        for mode in (O.WITH_REPLACEMENT, O.WITHOUT_REPLACEMENT):
+            law = E.draft_tree_law(ver, par, m, 1.0, mode, mode)
+            d = E.law_distance(law, tl)
+            assert d < 1e-12, (ver.__name__, mode, d)
+
+
+def pin_lossless_irregular_T07():
+    """Same check on an irregular tree (3 children at the root, 2 below the
+    first) at temperature 0.7, V = 4."""
+    m = W.ContextModel(4, seed=3)
+    par = np.array([-1, 0, 0, 0, 1, 1], np.int32)
+    T = np.float32(0.7)
+    tl = E.target_law(m, T, 3)
+    for mode in (O.WITH_REPLACEMENT, O.WITHOUT_REPLACEMENT):
+        law = E.draft_tree_law(O.verify_tree, par, m, T, mode, mode)
+        d = E.law_distance(law, tl)
+        assert d < 1e-12, (mode, d)
+
+
+def pin_chain_optimality():
+    """Theorem thm:chain_op and App. B: on a chain, E[tau] equals the draft
+    expectation of sum_l p^ini(alpha_l), and P(tau >= l | X^l = alpha^l) equals
+    p^ini(alpha_l); the token-level verifier does not do better."""
+    V, depth = 3, 3
+    m = W.ContextModel(V, seed=5)
+    par = W.chain_parents(depth)
+    e_tv = e_tl = e_pini = 0.0
+    ge = {}      # (prefix) -> [sum P(tree) P(tau >= l), sum P(tree) p_ini]
+    for tokens, ptree in E._draft_trees(par, m, 1.0, O.WITH_REPLACEMENT):
+        zb, zs = E.tree_rows(par, tokens, m)
+        br = E.decision_branches(
+            lambda d: O.verify_tree(par, tokens, zb, zs, 1.0, None, O.WITH_REPLACEMENT,
+                                    decide=d))
+        e_tv += ptree * sum(w * r.accept_len for w, r in br)
+        e_tl += ptree * E.expected_accept_len(O.verify_tree_tokenlevel, par, tokens, zb, zs,
+                                              1.0, O.WITH_REPLACEMENT)
+        pini = br[0][1].p_init
+        e_pini += ptree * float(pini[1:].sum())
+        for l in range(1, depth + 1):
+            key = tuple(tokens[1:l + 1])
+            acc = ge.setdefault(key, [0.0, 0.0])
+            acc[0] += ptree * sum(w for w, r in br if r.accept_len >= l)
+            acc[1] += ptree * pini[l]
+    assert abs(e_tv - e_pini) < 1e-12, (e_tv, e_pini)
+    assert e_tv >= e_tl - 1e-12, (e_tv, e_tl)
+    for key, (a, b) in ge.items():
+        assert abs(a - b) < 1e-12, (key, a, b)
+
+
+def pin_identical_models():
+    """M_s = M_b: every chain rate is 1, so the first leaf is accepted at once
+    and Y comes from that leaf's target row."""
+    rng = np.random.default_rng(11)
+    par = W.binary_parents(3)
+    n1, V = len(par), 17
+    z = rng.normal(0, 2, (n1, V))
+    tok = rng.integers(0, V, n1).astype(np.int32)
+    u = W.uniforms_np(rng, n1)
+    r = O.verify_tree(par, tok, z, z.copy(), 1.0, u, O.WITH_REPLACEMENT)
+    assert r.status == O.TREE_OK
+    assert np.all(r.p_init == 1.0)
+    assert r.accepted_node == 7 and r.test_order == [7]
+    np.testing.assert_allclose(r.y_weights, O.tempered_softmax(z[7], 1.0), atol=0)
+
+
+def pin_depth1_equals_rrsw():
+    """A root with leaf children only: p(root) = 1 makes Eq. (e1)-(e3) reduce to
+    Algorithm 2, so both verifiers give identical decisions, thresholds and Y."""
+    rng = np.random.default_rng(12)
+    for trial in range(40):
+        V = 50
+        k = int(rng.integers(1, 6))
+        par = np.array([-1] + [0] * k, np.int32)
+        zb = rng.normal(0, 2, (k + 1, V))
+        zs = zb + rng.normal(0, 1, (k + 1, V))
+        mode = int(trial % 2)
+        tok = np.concatenate([[0], rng.choice(V, k, replace=mode == O.WITH_REPLACEMENT)]) \
+            .astype(np.int32)
+        u = W.uniforms_np(rng, k + 1)
+        a = O.verify_tree(par, tok, zb, zs, 1.0, u, mode)
+        b = O.verify_tree_tokenlevel(par, tok, zb, zs, 1.0, u, mode)
+        assert a.accepted_node == b.accepted_node and a.bonus_token == b.bonus_token
+        assert a.test_order == b.test_order
+        assert np.array_equal(a.node_theta, b.node_theta)
+
+
+def pin_invariants():
+    """Along random traversals: 0 <= p' <= p at every update (Eq. e3 with
+    S <= p), the residual sums to one and is zero on the rejected token (Eq. e1),
+    and the draft update keeps a distribution (Eq. e2)."""
+    rng = np.random.default_rng(13)
+    V = 40
+    for _ in range(200):
+        b = rng.dirichlet(np.ones(V))
+        s = rng.dirichlet(np.ones(V))
+        p = float(rng.uniform(0.05, 1.0))
+        x = int(np.argmax(s / b))            # a token with p*b(x) < s(x)
+        d, S = O.residual_e1(p, b, s)
+        assert S <= p + 1e-15
+        if S == 0.0:     # p*b <= s everywhere: the parent can no longer be accepted
+            assert np.all(p * b <= s)
+            continue
+        pn = O.acceptance_update_e3(S, p)
+        assert 0.0 <= pn <= p + 1e-15
+        bn = d / S
+        assert abs(bn.sum() - 1.0) < 1e-12 and bn[x] == 0.0
+        sn = O.draft_update_e2(s, x)
+        assert sn[x] == 0.0 and abs(sn.sum() - 1.0) < 1e-12
+
+
+FAST_PINS = [pin_worked_example_trace, pin_worked_example_tokenlevel, pin_worked_example_law,
+             pin_single_token_table1, pin_rrsw_example, pin_tempered_softmax_inverse,
+             pin_inverse_cdf_law, pin_identical_models, pin_depth1_equals_rrsw,
+             pin_invariants]
+ENUM_PINS = [pin_lossless_exact, pin_lossless_irregular_T07, pin_chain_optimality]
+ALL_PINS = FAST_PINS + ENUM_PINS
+
+
+def first_failure(pins=ALL_PINS):
+    """Name of the first pin that fails (or raises), or None."""
+    for pin in pins:
+        try:
+            pin()
+        except Exception:          # noqa: BLE001 - any failure counts
+            return pin.__name__
+    return None

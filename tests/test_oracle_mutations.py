@@ -1,0 +1,157 @@
+"""Power of the oracle's pins: plant a plausible mistake in one step of the
+oracle (on the CPU, via monkeypatch) and check that some pin fails."""
+
+import numpy as np
+import pytest
+
+import oracle.tv_oracle as O
+import oracle_pins as P
+
+
+def _e1_without_p(p, b, s):
+    d = np.maximum(b - s, 0.0)
+    return d, float(d.sum())
+
+
+def _e1_swapped(p, b, s):
+    d = np.maximum(p * s - b, 0.0)
+    return d, float(d.sum())
+
+
+def _e2_no_renorm(s, x):
+    s = s.copy()
+    s[x] = 0.0
+    return s
+
+
+def _e2_wrong_token(s, x):
+    s = s.copy()
+    s[(x + 1) % len(s)] = 0.0
+    return s / s.sum()
+
+
+def _e2_always(s, x):
+    return _e2_orig(s, x)
+
+
+_e2_orig = O.draft_update_e2
+
+
+def _e3_plus_p(S, p):
+    return S / (S + p)
+
+
+def _e3_no_missing_mass(S, p):
+    return S / (S + 1.0)
+
+
+def _rate_swapped(p, b, s, x):
+    if p == 0.0 or s[x] == 0.0:
+        return 0.0
+    return min(p * s[x] / b[x], 1.0)
+
+
+def _rate_no_clip(p, b, s, x):
+    if p == 0.0 or b[x] == 0.0:
+        return 0.0
+    return p * b[x] / s[x]
+
+
+def _no_rerate(*args):
+    return None
+
+
+def _softmax_no_temperature(z, T):
+    return _softmax_orig(z, 1.0)
+
+
+_softmax_orig = O.tempered_softmax
+
+
+def _structure_reversed(parents, tokens, V, mode):
+    st, children, depth = _structure_orig(parents, tokens, V, mode)
+    if children is not None:
+        children = [list(reversed(c)) for c in children]
+    return st, children, depth
+
+
+_structure_orig = O._structure
+
+
+def _residual_without_norm(b, s):
+    return np.maximum(b - s, 0.0)
+
+
+MUTATIONS = {
+    "e1 drops the p factor": ("residual_e1", _e1_without_p),
+    "e1 target and draft swapped": ("residual_e1", _e1_swapped),
+    "e2 does not renormalise": ("draft_update_e2", _e2_no_renorm),
+    "e2 zeroes the wrong token": ("draft_update_e2", _e2_wrong_token),
+    "e3 denominator S + p": ("acceptance_update_e3", _e3_plus_p),
+    "e3 drops the missing mass": ("acceptance_update_e3", _e3_no_missing_mass),
+    "chain rate ratio inverted": ("chain_rate", _rate_swapped),
+    "chain rate not clipped at 1": ("chain_rate", _rate_no_clip),
+    "no re-rating after an update": ("rerate_chains", _no_rerate),
+    "temperature ignored": ("tempered_softmax", _softmax_no_temperature),
+    "children visited last-first": ("_structure", _structure_reversed),
+    "RRS residual not normalised": ("rrs_residual", _residual_without_norm),
+}
+
+
+def test_unmutated_oracle_passes_every_pin():
+    assert P.first_failure() is None
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(monkeypatch, name):
+    attr, fn = MUTATIONS[name]
+    monkeypatch.setattr(O, attr, fn)
+    assert P.first_failure() is not None, f"no pin catches: {name}"
+
+
+def test_mismatched_sibling_pairing_is_not_lossless(monkeypatch):
+    """Negative control for the sibling-mode reading: children drawn i.i.d. but
+    verified with Eq. (e2) (duplicates allowed through) must break losslessness,
+    while the matched pairings pass (pin_lossless_exact)."""
+    import oracle.enumerate as E
+    import workloads as W
+    monkeypatch.setattr(O, "_structure",
+                        lambda p, t, V, mode: _structure_orig(p, t, V, O.WITH_REPLACEMENT))
+    m = W.ContextModel(3, seed=0)
+    par = W.binary_parents(2)
+    law = E.draft_tree_law(O.verify_tree, par, m, 1.0, O.WITH_REPLACEMENT,
+                           O.WITHOUT_REPLACEMENT)
+    assert E.law_distance(law, E.target_law(m, 1.0, 3)) > 1e-4
+
+
+def test_two_leaf_sibling_counterexample(monkeypatch):
+    """Root with two leaf children drawn i.i.d. from q = [.6,.3,.1], target
+    [.3,.4,.3] (the Table 1 pair): the first-token law is the target with the
+    matched update and [3/10, 17/50, 9/25] when Eq. (e2) zeroes a duplicate."""
+    import oracle.enumerate as E
+
+    class M:
+        vocab = 3
+
+        def target(self, ctx):
+            return np.log([.3, .4, .3])
+
+        def draft(self, ctx):
+            return np.log([.6, .3, .1])
+
+    par = np.array([-1, 0, 0], np.int32)
+
+    def first_token(law):
+        out = np.zeros(3)
+        for seq, pr in law.items():
+            out[seq[0]] += pr
+        return out
+
+    good = first_token(E.draft_tree_law(O.verify_tree, par, M(), 1.0, O.WITH_REPLACEMENT,
+                                        O.WITH_REPLACEMENT, length=1))
+    np.testing.assert_allclose(good, [.3, .4, .3], atol=1e-12)
+    monkeypatch.setattr(O, "_structure",
+                        lambda p, t, V, mode: _structure_orig(p, t, V, O.WITH_REPLACEMENT))
+    bad = first_token(E.draft_tree_law(O.verify_tree, par, M(), 1.0, O.WITH_REPLACEMENT,
+                                       O.WITHOUT_REPLACEMENT, length=1))
+    np.testing.assert_allclose(bad, [3 / 10, 17 / 50, 9 / 25], atol=1e-12)
