@@ -1,0 +1,265 @@
+"""Benchmark of batched Traversal Verification on one MI355X.
+
+Workload: 256 trees x 64 draft nodes (65 rows per tree; irregular BFS trees of
+depth 7, branching 1-4 with P(k) proportional to 2^-k), V = 128256, bfloat16
+target and draft logits (target N(0, 3^2) plus +6 on 1% of the ids per row,
+draft = target + N(0, 1.5^2)), temperature 1, children drawn from the draft
+without replacement (the paper's sibling mode). Every step uses fresh seeds; the
+inputs are generated on the GPU outside the timed region (about 8.5 GB of
+logits per step).
+
+A step is one tv_verify call over the whole batch. The timed region holds
+exactly --steps calls, each bracketed by HIP events on the stream the kernel
+runs on, with the device synchronised before and after. Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
+CFG = 5
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "tv_verify_cfg5_hbm_counters.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2505_12398_amd", "csrc", "tv_kernels.hip")
+METRIC = ("verified trees/sec + achieved HBM GB/s (% peak), 64-node trees, V=128256, bf16")
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the kernel as it is now; else None."""
+    if not os.path.exists(PROFILE_COUNTERS):
+        return None
+    text = open(PROFILE_COUNTERS).read()
+    m = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m or not t or m.group(1) != kernel_hash():
+        return None
+    return float(t.group(1))
+
+
+def algorithmic_bytes(counters, vocab, elem_bytes, num_nodes):
+    """Bytes the method must move for one launch: both rows of every consulted
+    node, the accepted leaf's target row, both rows again per residual update,
+    plus the per-node inputs and outputs."""
+    c = counters.sum(dim=0).tolist()
+    row = vocab * elem_bytes
+    B = counters.shape[0]
+    small = B * num_nodes * (4 + 4 + 4 + 1 + 4) + B * 4 * (4 + TV_NUM_COUNTERS)
+    return {
+        "compulsory": 2 * row * c[0] + row * c[2],
+        "rescan": 2 * row * c[1],
+        "small": small,
+        "total": 2 * row * c[0] + row * c[2] + 2 * row * c[1] + small,
+    }
+
+
+TV_NUM_COUNTERS = 4
+
+
+def cpu_baseline(batch, gpu_out, sample: int, workers: int):
+    """The oracle on the first `sample` trees of one step, on host cores, with
+    parity of those trees against the GPU outputs."""
+    import multiprocessing as mp
+
+    import numpy as np
+
+    import workloads as W
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity  # noqa: E402  (test infrastructure: oracle comparison)
+
+    trees = [W.tree_numpy(batch, b) for b in range(sample)]
+    T = batch["temperature"]
+    mode = batch["mode"]
+    args = [(t, T, mode) for t in trees]
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(workers) as pool:
+        refs = pool.map(_oracle_one, args)
+    dt = time.perf_counter() - t0
+    g = parity.host_outputs(gpu_out)
+    rep = parity.ParityReport()
+    for b, ref in enumerate(refs):
+        kind, msg, worst = parity.compare_tree(g, b, ref, False, False, "bf16")
+        rep.trees += 1
+        rep.max_theta_rel = max(rep.max_theta_rel, worst[0])
+        rep.max_theta_abs = max(rep.max_theta_abs, worst[1])
+        if kind == "exact":
+            rep.exact += 1
+        elif kind == "near_tie":
+            rep.near_ties += 1
+        else:
+            rep.failures.append(f"tree {b}: {msg}")
+    return sample / dt, dt, rep
+
+
+def _oracle_one(args):
+    (par, tok, zb, zs, u), T, mode = args
+    from oracle import verify_tree
+    return verify_tree(par, tok, zb, zs, T, u, mode)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--cpu-sample", type=int, default=48,
+                    help="trees of one step verified by the CPU oracle (0: skip)")
+    ap.add_argument("--cpu-workers", type=int, default=0)
+    ap.add_argument("--mode", choices=["without", "with"], default="without")
+    ap.add_argument("--tokenlevel-steps", type=int, default=20)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the verification of independent trees needs no "
+              "collectives, and only --gpus 1 is supported in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2505_12398_amd as tv
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    tv.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    mode = W.WITHOUT_REPLACEMENT if args.mode == "without" else W.WITH_REPLACEMENT
+    cfg = W.CONFIGS[CFG]
+    B, n1, V = cfg.batch, cfg.n_nodes + 1, cfg.vocab
+    elem = 2
+    stream = torch.cuda.current_stream(dev)
+
+    def one_step(step, tokenlevel=False):
+        batch = W.make_batch(CFG, step=step, device=dev, mode=mode, seed=1)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"],
+                              batch["draft"], batch["temperature"], batch["uniforms"], mode,
+                              tokenlevel=tokenlevel, want_nodes=False, want_counters=True,
+                              stream=stream.cuda_stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1), batch, out
+
+    for w in range(args.warmup):
+        one_step(10_000 + w)
+        print(f"warmup {w + 1}/{args.warmup}", file=sys.stderr, flush=True)
+
+    times, nbytes, acc_tv, statuses = [], [], [], []
+    last = None
+    for s in range(args.steps):
+        ms, batch, out = one_step(s)
+        times.append(ms)
+        nb = algorithmic_bytes(out.counters, V, elem, n1)
+        nbytes.append(nb)
+        acc_tv.append(out.accept_len.float().mean().item() + 1.0)
+        statuses.append(int((out.status != tv.TV_TREE_OK).sum().item()))
+        if s == args.steps - 1:
+            last = (batch, out)
+        if (s + 1) % 10 == 0:
+            print(f"step {s + 1}/{args.steps}: {ms:.3f} ms", file=sys.stderr, flush=True)
+
+    ms_mean = sum(times) / len(times)
+    srt = sorted(times)
+    alg_total = sum(b["total"] for b in nbytes) / len(nbytes)
+    achieved = alg_total / (ms_mean * 1e-3) / 1e9
+    traffic = measured_traffic()
+
+    # token-level baseline on the same trees and uniforms (common random numbers)
+    tl_times, acc_tl, acc_tv_same = [], [], []
+    for s in range(args.tokenlevel_steps):
+        ms, batch, out = one_step(s, tokenlevel=True)
+        tl_times.append(ms)
+        acc_tl.append(out.accept_len.float().mean().item() + 1.0)
+        acc_tv_same.append(acc_tv[s] if s < len(acc_tv) else float("nan"))
+
+    res = {
+        "metric": METRIC,
+        "value": B / (ms_mean * 1e-3),
+        "unit": "trees/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_mean,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 terms, f64 accumulation and state (bf16 inputs)",
+        "data": "synthetic (seeded, generated on the GPU; fresh seeds every step)",
+        "config": {
+            "workload": cfg.name + " (256 trees x 65 rows x V=128256 bf16 target+draft, "
+                        "T=1, siblings without replacement)" if mode == W.WITHOUT_REPLACEMENT
+            else cfg.name + " (siblings i.i.d.)",
+            "batch": B, "rows_per_tree": n1, "vocab": V, "input_dtype": "bf16",
+            "temperature": cfg.temperature, "mode": args.mode + "_replacement",
+            "parallelism": "single GPU, one workgroup per tree",
+        },
+        "ms_p50": srt[len(srt) // 2],
+        "ms_p90": srt[min(len(srt) - 1, int(0.9 * len(srt)))],
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg_total,
+            "kernel": "verify_kernel<uint16_t> (tv_verify)",
+        },
+        "nominal_input_GBps": 2 * B * n1 * V * elem / (ms_mean * 1e-3) / 1e9,
+        "trees_with_error_status": sum(statuses),
+        "accept_len_mean": {
+            "traversal": sum(acc_tv) / len(acc_tv),
+            "tokenlevel": sum(acc_tl) / max(1, len(acc_tl)),
+            "traversal_same_steps": sum(acc_tv_same) / max(1, len(acc_tv_same)),
+        },
+        "tokenlevel_ms_per_step": sum(tl_times) / max(1, len(tl_times)),
+    }
+    if acc_tl:
+        res["accept_len_mean"]["delta_pct"] = 100.0 * (
+            res["accept_len_mean"]["traversal_same_steps"] / res["accept_len_mean"]["tokenlevel"]
+            - 1.0)
+
+    if args.cpu_sample > 0 and last is not None:
+        workers = args.cpu_workers or min(16, os.cpu_count() or 1)
+        sample = min(args.cpu_sample, B)
+        batch, _ = last
+        out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"],
+                              batch["draft"], batch["temperature"], batch["uniforms"], mode,
+                              want_nodes=True, want_counters=True)
+        torch.cuda.synchronize()
+        tps, secs, rep = cpu_baseline(batch, out, sample, workers)
+        res["cpu_baseline"] = {
+            "value": tps, "unit": "trees/s", "cores": workers, "kind": "oracle",
+            "sample": f"first {sample} trees of timed step {args.steps - 1} "
+                      f"({secs:.1f} s wall, float64 numpy, one process per core)",
+        }
+        res["parity_sample"] = {"trees": rep.trees, "exact": rep.exact,
+                                "near_ties": rep.near_ties, "failures": len(rep.failures),
+                                "max_theta_rel_err": rep.max_theta_rel,
+                                "max_theta_abs_err": rep.max_theta_abs}
+        if rep.failures:
+            print("\n".join(rep.failures[:5]), file=sys.stderr)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

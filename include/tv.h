@@ -1,0 +1,186 @@
+/*
+ * tv.h -- batched verification of speculative token trees on MI355X (gfx950).
+ *
+ * Traversal Verification (arXiv 2505.12398, Sec. 3.1, Algorithm 3) and the
+ * top-down token-level baseline (Sec. 2.2: recursive rejection sampling,
+ * Algorithm 2, applied layer by layer) for a batch of independent trees.
+ *
+ * Problem statement (Alg. 3 REQUIRE; Def. de_tree and Def. def2 in Sec. 3.3):
+ * a tree of drafted tokens rooted at the prefix X_0, the draft model's
+ * next-token distribution at every node that has children, the target model's
+ * next-token distribution at every node; the output is an accepted chain
+ * X^tau = (X_0, ..., X_tau) from the root plus one extra token Y, distributed
+ * exactly as the target model would have generated them.
+ *
+ * Conventions shared by both verifiers (the paper leaves them open):
+ *   - nodes are numbered so that parents[i] < i; node 0 is the root;
+ *   - children are ordered by ascending node index (Alg. 3 takes "the first
+ *     leaf" in this order, i.e. post-order DFS, App. E);
+ *   - row i of a logits tensor is the next-token distribution after the path
+ *     root..i; a child's acceptance ratio uses its parent's rows;
+ *   - the distributions are softmax(logits / T) with the same temperature T
+ *     for target and draft;
+ *   - uniforms[b][i] (i >= 1) is the uniform that tests node i, accepted iff
+ *     u < theta; uniforms[b][0] draws Y by inverse CDF in ascending token
+ *     order (the smallest y with u * W < C(y), C the running sum, W its total).
+ *
+ * Memory and streams. Every pointer is a device pointer. The caller owns all
+ * buffers; the library allocates nothing, keeps no state between calls and
+ * never synchronises the host: work is enqueued on `stream` and the call
+ * returns. Inputs are read-only. Outputs are written for every tree, including
+ * trees whose status is not TV_TREE_OK (they get -1 sentinels). Calls that
+ * write the same output buffers must be ordered by the caller.
+ *
+ * Errors. Argument problems the host can see (null pointers, sizes, enums,
+ * temperature, misaligned pointers) return a tv_status_t other than TV_OK and
+ * enqueue nothing. Problems in the data (a bad tree, non-finite logits) are
+ * reported per tree in status[b]. A failed kernel launch returns TV_ERR_HIP.
+ */
+#ifndef TV_H
+#define TV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum tv_status {
+  TV_OK = 0,
+  TV_ERR_INVALID_ARG = 1,  /* null pointer, negative size, unknown enum, T <= 0 or not finite */
+  TV_ERR_UNSUPPORTED = 2,  /* size or temperature beyond the limits below, or target and draft
+                              pointers whose addresses differ modulo 16 bytes */
+  TV_ERR_WORKSPACE = 3,    /* workspace smaller than tv_workspace_size() or misaligned */
+  TV_ERR_HIP = 4           /* the kernel launch failed (hipGetLastError) */
+} tv_status_t;
+
+typedef enum tv_dtype {
+  TV_DTYPE_BF16 = 0,       /* bfloat16 logits (uint16 bit patterns) */
+  TV_DTYPE_F32 = 1         /* float32 logits */
+} tv_dtype_t;
+
+/*
+ * How the children of a node were drawn from its draft distribution
+ * (Def. de_tree allows both). The draft update after a rejection must match:
+ *   WITHOUT_REPLACEMENT -- siblings drawn one after another without
+ *     replacement; a rejected token's draft probability is set to zero and the
+ *     rest renormalised (Eq. e2; the blue lines of Algorithm 2). Siblings must
+ *     carry distinct tokens (else status TV_TREE_DUP_SIBLING).
+ *   WITH_REPLACEMENT -- siblings drawn i.i.d.; the draft distribution stays as
+ *     it is after a rejection.
+ */
+typedef enum tv_sibling_mode {
+  TV_SIBLINGS_WITHOUT_REPLACEMENT = 0,
+  TV_SIBLINGS_WITH_REPLACEMENT = 1
+} tv_sibling_mode_t;
+
+/* Per-tree status written to status[b]. */
+enum {
+  TV_TREE_OK = 0,
+  TV_TREE_BAD_PARENT = 1,  /* parents[b][0] != -1, or parents[b][i] outside [0, i) */
+  TV_TREE_BAD_TOKEN = 2,   /* tokens[b][i] outside [0, vocab) for some i >= 1 */
+  TV_TREE_DUP_SIBLING = 3, /* two siblings share a token in WITHOUT_REPLACEMENT mode */
+  TV_TREE_NONFINITE = 4,   /* a row the verifier read holds NaN or +inf or no finite value,
+                              or a drafted token has draft logit -inf */
+  TV_TREE_DEGENERATE = 5   /* a residual distribution the algorithm samples from has zero
+                              mass in floating point (impossible in exact arithmetic) */
+};
+
+/* Values written to node_state[b][i]. */
+enum {
+  TV_NODE_UNTESTED = 0,    /* never compared against its uniform */
+  TV_NODE_ACCEPTED = 1,    /* the accepted node (Traversal Verification marks only the
+                              last node of X^tau; the token-level verifier marks every
+                              accepted node on the path). A root accepted with tau = 0
+                              is marked too. */
+  TV_NODE_REJECTED = 2,    /* tested and rejected */
+  TV_NODE_PRUNED = 3       /* discarded untested because its parent's acceptance rate
+                              had dropped to exactly 0 (Sec. 3.2 example) */
+};
+
+/* Limits of this implementation. */
+#define TV_MAX_NODES 1024          /* num_nodes = N + 1 (root included) */
+#define TV_MAX_VOCAB (1 << 20)
+#define TV_MIN_TEMPERATURE 1.0e-3f
+#define TV_MAX_TEMPERATURE 1.0e3f
+#define TV_NUM_COUNTERS 4
+
+/*
+ * Bytes of device workspace tv_verify / tv_verify_tokenlevel need for these
+ * sizes (0 means none; pass workspace = NULL then). Returns 0 for invalid
+ * sizes too.
+ */
+size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab);
+
+/*
+ * Traversal Verification, Algorithm 3 (Sec. 3.1) with Eq. (e1)-(e3), on
+ * `batch` independent trees of `num_nodes` = N + 1 nodes each.
+ *
+ * Inputs (device, row-major, contiguous):
+ *   parents        int32 [batch][num_nodes]   parents[b][0] = -1, 0 <= parents[b][i] < i
+ *   tokens         int32 [batch][num_nodes]   drafted token of node i (tokens[b][0] unused)
+ *   target_logits  dtype [batch][num_nodes][vocab]   target model logits per node
+ *   draft_logits   dtype [batch][num_nodes][vocab]   draft model logits per node; rows of
+ *                  nodes without children are never read
+ *   dtype          TV_DTYPE_BF16 or TV_DTYPE_F32 (both logits tensors)
+ *   temperature    T, applied to both models; finite, in [TV_MIN_TEMPERATURE, TV_MAX_TEMPERATURE]
+ *   uniforms       float32 [batch][num_nodes], each in [0, 1)
+ *   mode           tv_sibling_mode_t
+ * Outputs (device):
+ *   accept_len     int32 [batch]   tau, the depth of the accepted node (0: root only)
+ *   accepted_node  int32 [batch]   index of the last node of X^tau (its ancestors are the path)
+ *   bonus_token    int32 [batch]   Y
+ *   status         int32 [batch]   TV_TREE_*
+ *   node_state     int8  [batch][num_nodes] or NULL   TV_NODE_*
+ *   node_theta     float [batch][num_nodes] or NULL   acceptance probability the node was
+ *                  tested with; 0 for pruned nodes, -1 for untested nodes
+ *   p_init         float [batch][num_nodes] or NULL   Alg. 3 initial chain rates p^ini.
+ *                  Asking for them makes the verifier read the rows of every node that
+ *                  has children, which the traversal itself may not need.
+ *   counters       int32 [batch][TV_NUM_COUNTERS] or NULL:
+ *                  [0] nodes whose target and draft rows were read for the traversal,
+ *                  [1] residual updates (Eq. e1-e3; one pass over both rows of the parent),
+ *                  [2] 1 if the accepted node has no children (its target row is read for Y),
+ *                  [3] nodes tested against their uniform
+ *   workspace      device buffer of at least tv_workspace_size() bytes, 256-byte aligned
+ *                  (NULL if that size is 0)
+ *   stream         HIP stream the work is enqueued on (NULL: the default stream)
+ * Returns a tv_status_t.
+ */
+int tv_verify(int32_t batch, int32_t num_nodes, int32_t vocab,
+              const int32_t* parents, const int32_t* tokens,
+              const void* target_logits, const void* draft_logits, int32_t dtype,
+              float temperature, const float* uniforms, int32_t mode,
+              int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
+              int32_t* status, int8_t* node_state, float* node_theta, float* p_init,
+              int32_t* counters, void* workspace, size_t workspace_bytes,
+              hipStream_t stream);
+
+/*
+ * Token-level tree verification (Sec. 2.2): starting at the root, the children
+ * of the current node are tested in index order with recursive rejection
+ * sampling (Algorithm 2; without replacement per `mode`); an accepted child
+ * becomes the current node; Y is drawn from the target at an accepted leaf or
+ * from the residual once every child of the current node is rejected.
+ * Same arguments and layouts as tv_verify; p_init, if not NULL, is filled with -1.
+ */
+int tv_verify_tokenlevel(int32_t batch, int32_t num_nodes, int32_t vocab,
+                         const int32_t* parents, const int32_t* tokens,
+                         const void* target_logits, const void* draft_logits, int32_t dtype,
+                         float temperature, const float* uniforms, int32_t mode,
+                         int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
+                         int32_t* status, int8_t* node_state, float* node_theta,
+                         float* p_init, int32_t* counters, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+
+/* Static, human-readable name of a tv_status_t value ("unknown status" otherwise). */
+const char* tv_status_string(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TV_H */

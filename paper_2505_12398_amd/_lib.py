@@ -1,0 +1,173 @@
+"""ctypes binding of libtv (include/tv.h). Argument marshalling only."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtv.so")
+
+TV_OK, TV_ERR_INVALID_ARG, TV_ERR_UNSUPPORTED, TV_ERR_WORKSPACE, TV_ERR_HIP = range(5)
+TV_DTYPE_BF16, TV_DTYPE_F32 = 0, 1
+TV_SIBLINGS_WITHOUT_REPLACEMENT, TV_SIBLINGS_WITH_REPLACEMENT = 0, 1
+(TV_TREE_OK, TV_TREE_BAD_PARENT, TV_TREE_BAD_TOKEN, TV_TREE_DUP_SIBLING, TV_TREE_NONFINITE,
+ TV_TREE_DEGENERATE) = range(6)
+TV_NODE_UNTESTED, TV_NODE_ACCEPTED, TV_NODE_REJECTED, TV_NODE_PRUNED = range(4)
+TV_MAX_NODES = 1024
+TV_MAX_VOCAB = 1 << 20
+TV_NUM_COUNTERS = 4
+
+
+class TvError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {tv_status_string(code)} (status {code})")
+        self.code = code
+
+
+_lib = None
+
+_VERIFY_ARGTYPES = [
+    ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,            # batch, num_nodes, vocab
+    ctypes.c_void_p, ctypes.c_void_p,                          # parents, tokens
+    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,          # target, draft, dtype
+    ctypes.c_float, ctypes.c_void_p, ctypes.c_int32,           # temperature, uniforms, mode
+    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,         # accept_len, node, bonus
+    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,         # status, node_state, theta
+    ctypes.c_void_p, ctypes.c_void_p,                          # p_init, counters
+    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,         # workspace, bytes, stream
+]
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libtv.so once. Raises if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing; build it with __graft_entry__.build()")
+        lib = ctypes.CDLL(path)
+        lib.tv_workspace_size.argtypes = [ctypes.c_int32] * 3
+        lib.tv_workspace_size.restype = ctypes.c_size_t
+        for name in ("tv_verify", "tv_verify_tokenlevel"):
+            fn = getattr(lib, name)
+            fn.argtypes = _VERIFY_ARGTYPES
+            fn.restype = ctypes.c_int
+        lib.tv_status_string.argtypes = [ctypes.c_int]
+        lib.tv_status_string.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def tv_status_string(code: int) -> str:
+    return load_library().tv_status_string(int(code)).decode()
+
+
+def tv_workspace_size(batch: int, num_nodes: int, vocab: int) -> int:
+    return int(load_library().tv_workspace_size(batch, num_nodes, vocab))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return TV_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return TV_DTYPE_F32
+    raise TypeError(f"logits must be bfloat16 or float32, got {t.dtype}")
+
+
+def _call(name, batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits, dtype,
+          temperature, uniforms, mode, accept_len, accepted_node, bonus_token, status,
+          node_state, node_theta, p_init, counters, workspace, workspace_bytes, stream):
+    fn = getattr(load_library(), name)
+    return int(fn(batch, num_nodes, vocab, _ptr(parents), _ptr(tokens), _ptr(target_logits),
+                  _ptr(draft_logits), dtype, float(temperature), _ptr(uniforms), mode,
+                  _ptr(accept_len), _ptr(accepted_node), _ptr(bonus_token), _ptr(status),
+                  _ptr(node_state), _ptr(node_theta), _ptr(p_init), _ptr(counters),
+                  _ptr(workspace), int(workspace_bytes), stream))
+
+
+def tv_verify(batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits, dtype,
+              temperature, uniforms, mode, accept_len, accepted_node, bonus_token, status,
+              node_state=None, node_theta=None, p_init=None, counters=None, workspace=None,
+              workspace_bytes=0, stream=None) -> int:
+    """C-ABI ``tv_verify``: pointers may be torch tensors or raw ints; returns the status."""
+    return _call("tv_verify", batch, num_nodes, vocab, parents, tokens, target_logits,
+                 draft_logits, dtype, temperature, uniforms, mode, accept_len, accepted_node,
+                 bonus_token, status, node_state, node_theta, p_init, counters, workspace,
+                 workspace_bytes, stream)
+
+
+def tv_verify_tokenlevel(batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits,
+                         dtype, temperature, uniforms, mode, accept_len, accepted_node,
+                         bonus_token, status, node_state=None, node_theta=None, p_init=None,
+                         counters=None, workspace=None, workspace_bytes=0, stream=None) -> int:
+    """C-ABI ``tv_verify_tokenlevel``; same arguments as :func:`tv_verify`."""
+    return _call("tv_verify_tokenlevel", batch, num_nodes, vocab, parents, tokens,
+                 target_logits, draft_logits, dtype, temperature, uniforms, mode, accept_len,
+                 accepted_node, bonus_token, status, node_state, node_theta, p_init, counters,
+                 workspace, workspace_bytes, stream)
+
+
+@dataclass
+class VerifyOutputs:
+    accept_len: object
+    accepted_node: object
+    bonus_token: object
+    status: object
+    node_state: object = None
+    node_theta: object = None
+    p_init: object = None
+    counters: object = None
+
+
+def verify_batch(parents, tokens, target_logits, draft_logits, temperature, uniforms, mode,
+                 tokenlevel=False, want_nodes=True, want_p_init=False, want_counters=True,
+                 out: VerifyOutputs | None = None, stream=None) -> VerifyOutputs:
+    """Allocate outputs (torch, same device) unless given, check shapes, call the
+    C entry point on the current stream and raise on a non-OK return."""
+    import torch
+    B, n1 = parents.shape
+    V = target_logits.shape[-1]
+    dev = target_logits.device
+    for name, t, shape in (("parents", parents, (B, n1)), ("tokens", tokens, (B, n1)),
+                           ("uniforms", uniforms, (B, n1)),
+                           ("target_logits", target_logits, (B, n1, V)),
+                           ("draft_logits", draft_logits, (B, n1, V))):
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+        if t.device != dev or not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous on {dev}")
+    if parents.dtype != torch.int32 or tokens.dtype != torch.int32:
+        raise TypeError("parents and tokens must be int32")
+    if uniforms.dtype != torch.float32:
+        raise TypeError("uniforms must be float32")
+    if draft_logits.dtype != target_logits.dtype:
+        raise TypeError("target and draft logits must share a dtype")
+    dtype = _dtype_code(target_logits)
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = VerifyOutputs(
+            accept_len=torch.empty(B, **i32), accepted_node=torch.empty(B, **i32),
+            bonus_token=torch.empty(B, **i32), status=torch.empty(B, **i32),
+            node_state=torch.empty((B, n1), dtype=torch.int8, device=dev) if want_nodes else None,
+            node_theta=torch.empty((B, n1), dtype=torch.float32, device=dev)
+            if want_nodes else None,
+            p_init=torch.empty((B, n1), dtype=torch.float32, device=dev) if want_p_init else None,
+            counters=torch.empty((B, TV_NUM_COUNTERS), **i32) if want_counters else None)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream if dev.type == "cuda" else None
+    fn = tv_verify_tokenlevel if tokenlevel else tv_verify
+    st = fn(B, n1, V, parents, tokens, target_logits, draft_logits, dtype, temperature,
+            uniforms, mode, out.accept_len, out.accepted_node, out.bonus_token, out.status,
+            out.node_state, out.node_theta, out.p_init, out.counters, None, 0, stream)
+    if st != TV_OK:
+        raise TvError(st, fn.__name__)
+    return out

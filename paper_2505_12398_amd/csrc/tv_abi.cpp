@@ -1,0 +1,109 @@
+// C-ABI entry points of libtv (declared in include/tv.h): argument validation
+// on the host, then one kernel launch on the caller's stream. Nothing here
+// touches the GPU before the arguments are known to be valid, so the
+// validation paths run on machines without a GPU.
+#include <math.h>
+#include <stdint.h>
+
+#include "tv.h"
+#include "tv_launch.h"
+
+namespace tv {
+
+int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (a.batch < 0 || a.num_nodes < 1 || a.vocab < 2) return TV_ERR_INVALID_ARG;
+  if (a.dtype != TV_DTYPE_BF16 && a.dtype != TV_DTYPE_F32) return TV_ERR_INVALID_ARG;
+  if (a.mode != TV_SIBLINGS_WITHOUT_REPLACEMENT && a.mode != TV_SIBLINGS_WITH_REPLACEMENT)
+    return TV_ERR_INVALID_ARG;
+  if (!(a.temperature > 0.0f) || !isfinite(a.temperature)) return TV_ERR_INVALID_ARG;
+  if (a.temperature < TV_MIN_TEMPERATURE || a.temperature > TV_MAX_TEMPERATURE)
+    return TV_ERR_UNSUPPORTED;
+  if (a.num_nodes > TV_MAX_NODES || a.vocab > TV_MAX_VOCAB) return TV_ERR_UNSUPPORTED;
+  if (a.batch == 0) return TV_OK;
+  if (!a.parents || !a.tokens || !a.target || !a.draft || !a.uniforms || !a.accept_len ||
+      !a.accepted_node || !a.bonus_token || !a.status)
+    return TV_ERR_INVALID_ARG;
+  const size_t esize = a.dtype == TV_DTYPE_BF16 ? 2 : 4;
+  const uintptr_t t = reinterpret_cast<uintptr_t>(a.target);
+  const uintptr_t d = reinterpret_cast<uintptr_t>(a.draft);
+  if (t % esize || d % esize) return TV_ERR_INVALID_ARG;
+  if ((t & 15) != (d & 15)) return TV_ERR_UNSUPPORTED;
+  const void* int_ptrs[] = {a.parents, a.tokens, a.uniforms, a.accept_len, a.accepted_node,
+                            a.bonus_token, a.status, a.node_theta, a.p_init, a.counters};
+  for (const void* p : int_ptrs)
+    if (reinterpret_cast<uintptr_t>(p) % 4) return TV_ERR_INVALID_ARG;
+  return TV_OK;
+}
+
+}  // namespace tv
+
+namespace {
+
+int verify_common(tv::Algo algo, int32_t batch, int32_t num_nodes, int32_t vocab,
+                  const int32_t* parents, const int32_t* tokens, const void* target_logits,
+                  const void* draft_logits, int32_t dtype, float temperature,
+                  const float* uniforms, int32_t mode, int32_t* accept_len,
+                  int32_t* accepted_node, int32_t* bonus_token, int32_t* status,
+                  int8_t* node_state, float* node_theta, float* p_init, int32_t* counters,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tv::VerifyArgs a{batch,       num_nodes,  vocab,  parents,  tokens,     target_logits,
+                   draft_logits, dtype,      temperature, uniforms, mode,  accept_len,
+                   accepted_node, bonus_token, status, node_state, node_theta, p_init,
+                   counters};
+  int st = tv::validate(a, workspace, workspace_bytes);
+  if (st != TV_OK || batch == 0) return st;
+  return tv::launch(a, algo, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab) {
+  (void)batch;
+  (void)num_nodes;
+  (void)vocab;
+  return 0;
+}
+
+int tv_verify(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
+              const int32_t* tokens, const void* target_logits, const void* draft_logits,
+              int32_t dtype, float temperature, const float* uniforms, int32_t mode,
+              int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
+              int32_t* status, int8_t* node_state, float* node_theta, float* p_init,
+              int32_t* counters, void* workspace, size_t workspace_bytes,
+              hipStream_t stream) {
+  return verify_common(tv::Algo::kTraversal, batch, num_nodes, vocab, parents, tokens,
+                       target_logits, draft_logits, dtype, temperature, uniforms, mode,
+                       accept_len, accepted_node, bonus_token, status, node_state, node_theta,
+                       p_init, counters, workspace, workspace_bytes, stream);
+}
+
+int tv_verify_tokenlevel(int32_t batch, int32_t num_nodes, int32_t vocab,
+                         const int32_t* parents, const int32_t* tokens,
+                         const void* target_logits, const void* draft_logits, int32_t dtype,
+                         float temperature, const float* uniforms, int32_t mode,
+                         int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
+                         int32_t* status, int8_t* node_state, float* node_theta,
+                         float* p_init, int32_t* counters, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  return verify_common(tv::Algo::kTokenLevel, batch, num_nodes, vocab, parents, tokens,
+                       target_logits, draft_logits, dtype, temperature, uniforms, mode,
+                       accept_len, accepted_node, bonus_token, status, node_state, node_theta,
+                       p_init, counters, workspace, workspace_bytes, stream);
+}
+
+const char* tv_status_string(int code) {
+  switch (code) {
+    case TV_OK: return "ok";
+    case TV_ERR_INVALID_ARG: return "invalid argument";
+    case TV_ERR_UNSUPPORTED: return "unsupported size, temperature or pointer alignment";
+    case TV_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case TV_ERR_HIP: return "HIP kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,169 @@
+"""Parity of the HIP verifiers against the CPU oracle, tree by tree.
+
+Rule: status, then the accept/reject decision of every node the oracle tested,
+in the oracle's order, then the accepted node, tau, Y and the counters must be
+identical. At the first decision that differs, the tree counts as a near-tie
+(and the rest of it is not compared) if the oracle's |u - theta| < 1e-6; for Y,
+if u*W lies within 1e-6*W of a CDF boundary. Any other difference is a
+failure. Acceptance probabilities (theta of tested nodes, p_init) must agree
+within 1e-5 relative for float32 logits and 2e-3 relative for bfloat16 logits
+(plus 1e-7 absolute for values near zero).
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+import paper_2505_12398_amd as tv
+import workloads as W
+from oracle import verify_tree, verify_tree_tokenlevel
+
+BAND = 1e-6
+THETA_RTOL = {"f32": 1e-5, "bf16": 2e-3}
+THETA_ATOL = 1e-7
+
+
+@dataclass
+class ParityReport:
+    trees: int = 0
+    exact: int = 0
+    near_ties: int = 0
+    failures: list = field(default_factory=list)
+    max_theta_rel: float = 0.0
+    max_theta_abs: float = 0.0
+
+    def add(self, other: "ParityReport"):
+        self.trees += other.trees
+        self.exact += other.exact
+        self.near_ties += other.near_ties
+        self.failures += other.failures
+        self.max_theta_rel = max(self.max_theta_rel, other.max_theta_rel)
+        self.max_theta_abs = max(self.max_theta_abs, other.max_theta_abs)
+
+    def summary(self):
+        return (f"{self.trees} trees: {self.exact} exact, {self.near_ties} near-ties, "
+                f"{len(self.failures)} failures, max theta err {self.max_theta_rel:.2e} rel "
+                f"{self.max_theta_abs:.2e} abs")
+
+
+def host_outputs(out: tv.VerifyOutputs):
+    def h(t):
+        return None if t is None else t.detach().cpu().numpy()
+    return {k: h(getattr(out, k)) for k in ("accept_len", "accepted_node", "bonus_token",
+                                             "status", "node_state", "node_theta", "p_init",
+                                             "counters")}
+
+
+def _theta_ok(g, r, rtol):
+    return abs(float(g) - float(r)) <= rtol * abs(float(r)) + THETA_ATOL
+
+
+def compare_tree(g: dict, b: int, ref, tokenlevel: bool, check_p_init: bool,
+                 dtype: str = "f32"):
+    """Returns (kind, message, (max_rel, max_abs) theta error) with kind in
+    exact/near_tie/fail."""
+    rtol = THETA_RTOL[dtype]
+    worst = [0.0, 0.0]
+    if int(g["status"][b]) != ref.status:
+        return "fail", f"status gpu {g['status'][b]} oracle {ref.status}", worst
+    if ref.status != tv.TV_TREE_OK:
+        ok = (g["accept_len"][b] == -1 and g["accepted_node"][b] == -1
+              and g["bonus_token"][b] == -1)
+        return ("exact", "", worst) if ok else ("fail", "error tree without sentinels", worst)
+    state, theta = g["node_state"][b], g["node_theta"][b]
+    for node in ref.test_order:
+        want = ref.node_state[node]
+        if state[node] != want:
+            if ref.margins[node] < BAND:
+                return "near_tie", f"node {node} margin {ref.margins[node]:.2e}", worst
+            return ("fail", f"node {node} state gpu {state[node]} oracle {want} "
+                    f"theta gpu {theta[node]:.9g} oracle {ref.node_theta[node]:.9g} "
+                    f"u-margin {ref.margins[node]:.2e}", worst)
+        th_r = float(ref.node_theta[node])
+        err = abs(float(theta[node]) - th_r)
+        worst[1] = max(worst[1], err)
+        if th_r != 0.0:
+            worst[0] = max(worst[0], err / abs(th_r))
+        if not _theta_ok(theta[node], th_r, rtol):
+            return "fail", f"node {node} theta gpu {theta[node]!r} oracle {th_r!r}", worst
+    if not np.array_equal(state.astype(np.int64), ref.node_state.astype(np.int64)):
+        return "fail", f"node states differ: gpu {state.tolist()} oracle {ref.node_state.tolist()}", worst
+    pruned = ref.node_state == tv.TV_NODE_PRUNED
+    if not np.all(theta[pruned] == 0.0):
+        return "fail", "pruned nodes must report theta 0", worst
+    untested = ref.node_state == tv.TV_NODE_UNTESTED
+    if not np.all(theta[untested] == -1.0):
+        return "fail", "untested nodes must report theta -1", worst
+    if int(g["accepted_node"][b]) != ref.accepted_node or int(g["accept_len"][b]) != ref.accept_len:
+        return ("fail", f"accepted gpu {g['accepted_node'][b]}/{g['accept_len'][b]} oracle "
+                f"{ref.accepted_node}/{ref.accept_len}", worst)
+    if g["counters"] is not None:
+        want = np.array(ref.counters)
+        if not np.array_equal(g["counters"][b], want):
+            return "fail", f"counters gpu {g['counters'][b].tolist()} oracle {want.tolist()}", worst
+    if check_p_init and g["p_init"] is not None and not tokenlevel:
+        for i, (a, r) in enumerate(zip(g["p_init"][b], ref.p_init)):
+            if not _theta_ok(a, r, rtol):
+                return "fail", f"p_init[{i}] gpu {a!r} oracle {r!r}", worst
+    if int(g["bonus_token"][b]) != ref.bonus_token:
+        if ref.y_margin < BAND:
+            return "near_tie", f"Y margin {ref.y_margin:.2e}", worst
+        return ("fail", f"Y gpu {g['bonus_token'][b]} oracle {ref.bonus_token} "
+                f"margin {ref.y_margin:.2e}", worst)
+    return "exact", "", worst
+
+
+def oracle_tree(batch: dict, b: int, tokenlevel: bool):
+    par, tok, zb, zs, u = W.tree_numpy(batch, b)
+    fn = verify_tree_tokenlevel if tokenlevel else verify_tree
+    return fn(par, tok, zb, zs, batch["temperature"], u, batch["mode"])
+
+
+def run_gpu(batch: dict, tokenlevel: bool, p_init: bool = False):
+    out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"], batch["draft"],
+                          batch["temperature"], batch["uniforms"], batch["mode"],
+                          tokenlevel=tokenlevel, want_p_init=p_init)
+    return host_outputs(out)
+
+
+def check(batch: dict, tokenlevel: bool, trees=None, p_init: bool = False,
+          gpu: dict | None = None, label: str = "") -> ParityReport:
+    """Run the HIP verifier on the whole batch (unless ``gpu`` outputs are
+    given) and compare the listed trees (all by default) with the oracle."""
+    if gpu is None:
+        gpu = run_gpu(batch, tokenlevel, p_init)
+    B = batch["parents"].shape[0]
+    rep = ParityReport()
+    for b in (range(B) if trees is None else trees):
+        ref = oracle_tree(batch, b, tokenlevel)
+        kind, msg, worst = compare_tree(gpu, b, ref, tokenlevel, p_init,
+                                        batch.get("dtype", "f32"))
+        rep.trees += 1
+        rep.max_theta_rel = max(rep.max_theta_rel, worst[0])
+        rep.max_theta_abs = max(rep.max_theta_abs, worst[1])
+        if kind == "exact":
+            rep.exact += 1
+        elif kind == "near_tie":
+            rep.near_ties += 1
+        else:
+            rep.failures.append(f"{label} tree {b}: {msg}")
+    return rep
+
+
+def from_numpy(parents, tokens, target, draft, uniforms, temperature, mode, device,
+               dtype="f32"):
+    """Batch dict from host arrays (target/draft float64 are cast to the dtype)."""
+    import torch
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    return {
+        "parents": torch.as_tensor(np.ascontiguousarray(parents), dtype=torch.int32,
+                                   device=device),
+        "tokens": torch.as_tensor(np.ascontiguousarray(tokens), dtype=torch.int32,
+                                  device=device),
+        "target": torch.as_tensor(np.asarray(target, np.float32), device=device).to(tdt),
+        "draft": torch.as_tensor(np.asarray(draft, np.float32), device=device).to(tdt),
+        "uniforms": torch.as_tensor(np.asarray(uniforms, np.float32), device=device),
+        "temperature": temperature, "mode": mode, "dtype": dtype,
+    }

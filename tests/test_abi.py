@@ -1,0 +1,120 @@
+"""The C-ABI library without a GPU: it loads, exports every function the
+header declares, agrees with the binding's constants, and rejects bad
+arguments on the host before any HIP call."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2505_12398_amd as tv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tv.h")
+
+
+def header_text():
+    with open(HEADER) as f:
+        return f.read()
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", header_text(), flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:size_t|int|const char\*)\s+(tv_\w+)\s*\(", text,
+                                 flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = tv.load_library()
+    names = declared_functions()
+    assert {"tv_verify", "tv_verify_tokenlevel", "tv_workspace_size",
+            "tv_status_string"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_constants_match_header():
+    text = header_text()
+
+    def define(name):
+        line = re.search(rf"#define {name}\s+([^\n]+)", text).group(1)
+        return line.split("/*")[0].strip()
+
+    assert eval(define("TV_MAX_NODES")) == tv.TV_MAX_NODES
+    assert eval(define("TV_MAX_VOCAB")) == tv.TV_MAX_VOCAB
+    assert eval(define("TV_NUM_COUNTERS")) == tv.TV_NUM_COUNTERS
+    for name in ["TV_OK", "TV_ERR_INVALID_ARG", "TV_ERR_UNSUPPORTED", "TV_ERR_WORKSPACE",
+                 "TV_ERR_HIP", "TV_DTYPE_BF16", "TV_DTYPE_F32", "TV_SIBLINGS_WITHOUT_REPLACEMENT",
+                 "TV_SIBLINGS_WITH_REPLACEMENT", "TV_TREE_OK", "TV_TREE_BAD_PARENT",
+                 "TV_TREE_BAD_TOKEN", "TV_TREE_DUP_SIBLING", "TV_TREE_NONFINITE",
+                 "TV_TREE_DEGENERATE", "TV_NODE_UNTESTED", "TV_NODE_ACCEPTED",
+                 "TV_NODE_REJECTED", "TV_NODE_PRUNED"]:
+        m = re.search(rf"\b{name}\s*=\s*(\d+)", text)
+        assert m and int(m.group(1)) == getattr(tv, name), name
+
+
+def test_status_strings():
+    assert tv.tv_status_string(tv.TV_OK) == "ok"
+    for code in range(1, 5):
+        assert tv.tv_status_string(code) not in ("ok", "unknown status")
+    assert tv.tv_status_string(99) == "unknown status"
+
+
+def test_workspace_size_is_zero():
+    assert tv.tv_workspace_size(256, 65, 128256) == 0
+
+
+# Fake, never-dereferenced device addresses: validation fails before any HIP call.
+A = 0x10000
+
+
+def call(fn="tv_verify", **kw):
+    args = dict(batch=2, num_nodes=5, vocab=100, parents=A, tokens=A, target_logits=A,
+                draft_logits=A + 0x1000, dtype=tv.TV_DTYPE_BF16, temperature=1.0, uniforms=A,
+                mode=0, accept_len=A, accepted_node=A, bonus_token=A, status=A)
+    args.update(kw)
+    return getattr(tv, fn)(**args)
+
+
+@pytest.mark.parametrize("fn", ["tv_verify", "tv_verify_tokenlevel"])
+@pytest.mark.parametrize("kw,want", [
+    (dict(batch=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(num_nodes=0), tv.TV_ERR_INVALID_ARG),
+    (dict(vocab=1), tv.TV_ERR_INVALID_ARG),
+    (dict(dtype=7), tv.TV_ERR_INVALID_ARG),
+    (dict(mode=2), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=0.0), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=-1.0), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=float("nan")), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=float("inf")), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=1e-5), tv.TV_ERR_UNSUPPORTED),
+    (dict(temperature=1e4), tv.TV_ERR_UNSUPPORTED),
+    (dict(num_nodes=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(vocab=tv.TV_MAX_VOCAB + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(parents=None), tv.TV_ERR_INVALID_ARG),
+    (dict(tokens=None), tv.TV_ERR_INVALID_ARG),
+    (dict(target_logits=None), tv.TV_ERR_INVALID_ARG),
+    (dict(draft_logits=None), tv.TV_ERR_INVALID_ARG),
+    (dict(uniforms=None), tv.TV_ERR_INVALID_ARG),
+    (dict(accept_len=None), tv.TV_ERR_INVALID_ARG),
+    (dict(accepted_node=None), tv.TV_ERR_INVALID_ARG),
+    (dict(bonus_token=None), tv.TV_ERR_INVALID_ARG),
+    (dict(status=None), tv.TV_ERR_INVALID_ARG),
+    (dict(target_logits=A + 1, draft_logits=A + 1), tv.TV_ERR_INVALID_ARG),
+    (dict(dtype=tv.TV_DTYPE_F32, target_logits=A + 2, draft_logits=A + 2),
+     tv.TV_ERR_INVALID_ARG),
+    (dict(target_logits=A + 2, draft_logits=A + 4), tv.TV_ERR_UNSUPPORTED),
+    (dict(parents=A + 2), tv.TV_ERR_INVALID_ARG),
+    (dict(counters=A + 1), tv.TV_ERR_INVALID_ARG),
+])
+def test_host_validation(fn, kw, want):
+    assert call(fn, **kw) == want
+
+
+@pytest.mark.parametrize("fn", ["tv_verify", "tv_verify_tokenlevel"])
+def test_empty_batch_is_a_no_op(fn):
+    # batch 0 with null buffers: valid, nothing enqueued, no HIP call
+    assert call(fn, batch=0, parents=None, tokens=None, target_logits=None, draft_logits=None,
+                uniforms=None, accept_len=None, accepted_node=None, bonus_token=None,
+                status=None) == tv.TV_OK
