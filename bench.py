@@ -121,6 +121,9 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=0)
     ap.add_argument("--mode", choices=["without", "with"], default="without")
     ap.add_argument("--tokenlevel-steps", type=int, default=20)
+    ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
+                    help="only run plain device-to-device copies of this size (to scale "
+                         "the FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -136,9 +139,18 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
-    tv.load_library()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration_gib > 0:
+        n = int(args.copy_calibration_gib * (1 << 30)) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": n * 4, "launches": 3}), flush=True)
+        return
+    tv.load_library()
     mode = W.WITHOUT_REPLACEMENT if args.mode == "without" else W.WITH_REPLACEMENT
     cfg = W.CONFIGS[CFG]
     B, n1, V = cfg.batch, cfg.n_nodes + 1, cfg.vocab
@@ -222,7 +234,7 @@ def main():
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_total,
-            "kernel": "verify_kernel<uint16_t> (tv_verify)",
+            "kernel": "verify_kernel<uint16_t, FastArith, 0> (tv_verify)",
         },
         "nominal_input_GBps": 2 * B * n1 * V * elem / (ms_mean * 1e-3) / 1e9,
         "trees_with_error_status": sum(statuses),

@@ -868,8 +868,8 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
 // The kernel: one workgroup per tree
 // ---------------------------------------------------------------------------
 
-template <typename T, class A>
-__global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar, int algo) {
+template <typename T, class A, int algo>
+__global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
   __shared__ TreeSmem sm;
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
@@ -1008,16 +1008,16 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar, int al
 // with few elements the per-element rounding of the fast path does not average.
 constexpr int kPreciseBelowVocab = 16384;
 
-template <typename T>
-int launch_dtype(const Params& P, bool precise, int batch, int algo, hipStream_t stream) {
+template <typename T, int algo>
+int launch_typed(const Params& P, bool precise, int batch, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(batch));
   const dim3 block(kThreads);
   if (precise) {
     PreciseArith ar{P.k64};
-    hipLaunchKernelGGL((verify_kernel<T, PreciseArith>), grid, block, 0, stream, P, ar, algo);
+    hipLaunchKernelGGL((verify_kernel<T, PreciseArith, algo>), grid, block, 0, stream, P, ar);
   } else {
     FastArith ar{P.k32};
-    hipLaunchKernelGGL((verify_kernel<T, FastArith>), grid, block, 0, stream, P, ar, algo);
+    hipLaunchKernelGGL((verify_kernel<T, FastArith, algo>), grid, block, 0, stream, P, ar);
   }
   return hipGetLastError() == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
@@ -1047,9 +1047,13 @@ int launch(const VerifyArgs& a, Algo algo, hipStream_t stream) {
   P.k64 = 1.4426950408889634 / static_cast<double>(a.temperature);
   P.k32 = static_cast<float>(P.k64);
   const bool precise = a.dtype == TV_DTYPE_F32 || a.vocab < kPreciseBelowVocab;
+  constexpr int kTv = static_cast<int>(Algo::kTraversal);
+  constexpr int kTl = static_cast<int>(Algo::kTokenLevel);
   if (a.dtype == TV_DTYPE_BF16)
-    return launch_dtype<uint16_t>(P, precise, a.batch, static_cast<int>(algo), stream);
-  return launch_dtype<float>(P, precise, a.batch, static_cast<int>(algo), stream);
+    return algo == Algo::kTraversal ? launch_typed<uint16_t, kTv>(P, precise, a.batch, stream)
+                                    : launch_typed<uint16_t, kTl>(P, precise, a.batch, stream);
+  return algo == Algo::kTraversal ? launch_typed<float, kTv>(P, precise, a.batch, stream)
+                                  : launch_typed<float, kTl>(P, precise, a.batch, stream);
 }
 
 }  // namespace tv
