@@ -103,7 +103,8 @@ enum {
 
 /* Limits of this implementation. */
 #define TV_MAX_NODES 1024          /* num_nodes = N + 1 (root included) */
-#define TV_MAX_VOCAB (1 << 20)
+#define TV_MAX_VOCAB (1 << 20)          /* bf16 logits */
+#define TV_MAX_VOCAB_F32 (1 << 19)      /* fp32 logits */
 #define TV_MIN_TEMPERATURE 1.0e-3f
 #define TV_MAX_TEMPERATURE 1.0e3f
 #define TV_NUM_COUNTERS 4
@@ -127,6 +128,7 @@ size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab);
  *                  nodes without children are never read
  *   dtype          TV_DTYPE_BF16 or TV_DTYPE_F32 (both logits tensors)
  *   temperature    T, applied to both models; finite, in [TV_MIN_TEMPERATURE, TV_MAX_TEMPERATURE]
+ *   vocab          2 .. TV_MAX_VOCAB (bf16) or TV_MAX_VOCAB_F32 (fp32)
  *   uniforms       float32 [batch][num_nodes], each in [0, 1)
  *   mode           tv_sibling_mode_t
  * Outputs (device):

@@ -14,7 +14,7 @@ from ._lib import (  # noqa: F401
     TV_TREE_OK, TV_TREE_BAD_PARENT, TV_TREE_BAD_TOKEN, TV_TREE_DUP_SIBLING,
     TV_TREE_NONFINITE, TV_TREE_DEGENERATE,
     TV_NODE_UNTESTED, TV_NODE_ACCEPTED, TV_NODE_REJECTED, TV_NODE_PRUNED,
-    TV_MAX_NODES, TV_MAX_VOCAB, TV_NUM_COUNTERS,
+    TV_MAX_NODES, TV_MAX_VOCAB, TV_MAX_VOCAB_F32, TV_NUM_COUNTERS,
     LIB_PATH, TvError, load_library,
     tv_workspace_size, tv_verify, tv_verify_tokenlevel, tv_status_string,
     VerifyOutputs, verify_batch,

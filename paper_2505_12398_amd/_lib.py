@@ -16,6 +16,7 @@ TV_SIBLINGS_WITHOUT_REPLACEMENT, TV_SIBLINGS_WITH_REPLACEMENT = 0, 1
 TV_NODE_UNTESTED, TV_NODE_ACCEPTED, TV_NODE_REJECTED, TV_NODE_PRUNED = range(4)
 TV_MAX_NODES = 1024
 TV_MAX_VOCAB = 1 << 20
+TV_MAX_VOCAB_F32 = 1 << 19
 TV_NUM_COUNTERS = 4
 
 

@@ -21,6 +21,7 @@ int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
   if (a.temperature < TV_MIN_TEMPERATURE || a.temperature > TV_MAX_TEMPERATURE)
     return TV_ERR_UNSUPPORTED;
   if (a.num_nodes > TV_MAX_NODES || a.vocab > TV_MAX_VOCAB) return TV_ERR_UNSUPPORTED;
+  if (a.dtype == TV_DTYPE_F32 && a.vocab > TV_MAX_VOCAB_F32) return TV_ERR_UNSUPPORTED;
   if (a.batch == 0) return TV_OK;
   if (!a.parents || !a.tokens || !a.target || !a.draft || !a.uniforms || !a.accept_len ||
       !a.accepted_node || !a.bonus_token || !a.status)

@@ -43,7 +43,7 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxNodes = TV_MAX_NODES;
-constexpr int kMaxBlocks = 4096;   // sampling blocks of 64 vectors (1 per wave-iteration)
+constexpr int kMaxBlocks = 2048;   // sampling blocks (64 * bmul vectors each)
 constexpr int kUnroll = 4;         // vectors per row in flight per lane
 
 enum : int { kCmdDone = 0, kCmdStats = 1, kCmdSPass = 2, kCmdSample = 3 };
@@ -51,7 +51,7 @@ enum : int {
   kPhDescend = 0, kPhTest, kPhAfterSPass, kPhFinal, kPhFinalLeafStats, kPhAfterSample,
   kPhPinit, kPhTlVisit, kPhTlAfterSPass
 };
-enum : uint8_t { kFlagStats = 1, kFlagConsulted = 2, kFlagLeafStats = 4 };
+enum : uint8_t { kFlagStats = 1, kFlagConsulted = 2, kFlagLeafStats = 4, kFlagSd = 8 };
 
 struct TreeSmem {
   // tree structure
@@ -71,20 +71,23 @@ struct TreeSmem {
   double A[kMaxNodes];               // residual target b = [A p - B q]_+
   double B[kMaxNodes];
   double rem[kMaxNodes];             // draft mass left after removing rejected tokens
-  double lsb[kMaxNodes];             // log2 of the target row sum
-  double lss[kMaxNodes];             // log2 of the draft row sum
   double pini[kMaxNodes];
+  double sdsum[kMaxNodes];           // sum of the draft row's terms in its frame
+  double invsb[kMaxNodes];           // 1 / (sum of the target row's terms)
+  double invss[kMaxNodes];           // 1 / (sum of the draft row's terms)
   double cb[kMaxNodes];              // exponent offset of the target row: -max * k
   double cs[kMaxNodes];              // exponent offset of the draft row
-  float gzb[kMaxNodes];              // parent's target logit at this node's token
-  float gzs[kMaxNodes];              // parent's draft logit at this node's token
+  // per-node, about the node's own token at its parent (set by the parent's STATS)
+  double r0[kMaxNodes];              // original ratio p(x) / q(x)
+  double et[kMaxNodes];              // draft term of x in the parent's frame
   // sampling
   double blocks[kMaxBlocks];
   // reductions
   double red_d[2 * kWaves];
   float red_f[2 * kWaves];
+  int gather_bad;
   // command issued by thread 0 for the whole workgroup
-  int cmd, cmd_node, cmd_two_rows, cmd_gather;
+  int cmd, cmd_node, cmd_two_rows, cmd_gather, cmd_sd;
   double cmd_ap, cmd_bp;             // multipliers of the target / draft terms
   double cmd_cb, cmd_cs;
   // pass results
@@ -170,29 +173,45 @@ __device__ inline float wave_max(float v) {
   return v;
 }
 
-// Sum of one double per thread; result valid in every thread.
-__device__ double block_sum(TreeSmem& sm, double v, int slot) {
+// Sums of two doubles per thread in one LDS round; results valid in every thread.
+__device__ __forceinline__ void block_sum2(TreeSmem& sm, double& a, double& b) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  v = wave_sum(v);
-  if (lane == 0) sm.red_d[slot * kWaves + wave] = v;
+  a = wave_sum(a);
+  b = wave_sum(b);
+  if (lane == 0) {
+    sm.red_d[wave] = a;
+    sm.red_d[kWaves + wave] = b;
+  }
   __syncthreads();
-  double t = 0.0;
+  double ta = 0.0, tb = 0.0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) t += sm.red_d[slot * kWaves + w];
+  for (int w = 0; w < kWaves; ++w) {
+    ta += sm.red_d[w];
+    tb += sm.red_d[kWaves + w];
+  }
   __syncthreads();
-  return t;
+  a = ta;
+  b = tb;
 }
 
-__device__ float block_max(TreeSmem& sm, float v, int slot) {
+__device__ __forceinline__ void block_max2(TreeSmem& sm, float& a, float& b) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  v = wave_max(v);
-  if (lane == 0) sm.red_f[slot * kWaves + wave] = v;
+  a = wave_max(a);
+  b = wave_max(b);
+  if (lane == 0) {
+    sm.red_f[wave] = a;
+    sm.red_f[kWaves + wave] = b;
+  }
   __syncthreads();
-  float t = -INFINITY;
+  float ta = -INFINITY, tb = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) t = fmaxf(t, sm.red_f[slot * kWaves + w]);
+  for (int w = 0; w < kWaves; ++w) {
+    ta = fmaxf(ta, sm.red_f[w]);
+    tb = fmaxf(tb, sm.red_f[kWaves + w]);
+  }
   __syncthreads();
-  return t;
+  a = ta;
+  b = tb;
 }
 
 // ---------------------------------------------------------------------------
@@ -224,95 +243,91 @@ struct PreciseArith {              // fp64 throughout
 // STATS: row maximum and sum of terms, online over one read of the row
 // ---------------------------------------------------------------------------
 
+// Running state of one thread over a row. Before the first finite value the
+// maximum is -inf and the frame is that of a finite sentinel, so -inf entries
+// add 2^-inf = 0 with no branch, a NaN or +inf entry turns the sum into NaN,
+// and a row with no finite entry keeps maximum -inf.
+constexpr float kFrameSentinel = -1.0e30f;
+
 struct Online {
   float m;     // running max
-  double c;    // frame of m
+  double c;    // frame of m (of the sentinel while m = -inf)
   double s;    // sum of terms in the frame c
 };
 
-template <class A, int N>
-__device__ inline void online_add(Online& o, const float (&x)[N], int n, const A& ar) {
-  float vmax = -INFINITY;
-#pragma unroll
-  for (int e = 0; e < N; ++e)
-    if (e < n) vmax = fmaxf(vmax, x[e]);
+template <class A>
+__device__ __forceinline__ Online online_init(const A& ar) {
+  return Online{-INFINITY, ar.frame(kFrameSentinel), 0.0};
+}
+
+// Raise the running maximum to at least vmax (rescaling the sum), then add the
+// terms of x[0..n).
+template <class A>
+__device__ __forceinline__ void online_raise(Online& o, float vmax, const A& ar) {
   if (vmax > o.m) {
     const double cn = ar.frame(vmax);
-    if (o.m != -INFINITY) o.s *= exp2(cn - o.c);
+    if constexpr (A::kPrecise) {
+      o.s *= exp2(cn - o.c);
+    } else {        // fp32 rescale: ~1e-7 relative, random across threads
+      o.s *= static_cast<double>(fast_exp2(static_cast<float>(cn - o.c)));
+    }
     o.m = vmax;
     o.c = cn;
   }
-  if (o.m == -INFINITY) {      // only -inf (or NaN) seen so far
-#pragma unroll
-    for (int e = 0; e < N; ++e)
-      if (e < n && x[e] != x[e]) o.s = NAN;
-    return;
-  }
+}
+
+template <class A, int N>
+__device__ __forceinline__ void online_sum(Online& o, const float (&x)[N], const A& ar) {
   if constexpr (A::kPrecise) {
 #pragma unroll
-    for (int e = 0; e < N; ++e)
-      if (e < n) o.s += ar.ex(x[e], o.c);
+    for (int e = 0; e < N; ++e) o.s += ar.ex(x[e], o.c);
   } else {
     const float cf = static_cast<float>(o.c);
     float part = 0.0f;
 #pragma unroll
-    for (int e = 0; e < N; ++e)
-      if (e < n) part += fast_exp2(fmaf(x[e], ar.k, cf));
+    for (int e = 0; e < N; ++e) part += fast_exp2(fmaf(x[e], ar.k, cf));
     o.s += static_cast<double>(part);
   }
 }
 
-// Combine the per-thread online states; thread 0 receives (max, frame, sum).
-template <class A>
-__device__ void finish_online(TreeSmem& sm, const Online& o, const A& ar, int slot, float* m_out,
-                              double* c_out, double* s_out) {
-  const float M = block_max(sm, o.m, slot);
-  const double C = ar.frame(M);
-  double s = 0.0;
-  if (o.m == -INFINITY) {
-    s = (o.s != o.s) ? static_cast<double>(NAN) : 0.0;
-  } else {
-    s = o.s * exp2(C - o.c);
-  }
-  s = block_sum(sm, s, slot);
-  if (threadIdx.x == 0) {
-    *m_out = M;
-    *c_out = C;
-    *s_out = s;
-  }
+template <int N>
+__device__ __forceinline__ float vec_max(const float (&x)[N]) {
+  float m = x[0];
+#pragma unroll
+  for (int e = 1; e < N; ++e) m = fmaxf(m, x[e]);
+  return m;
 }
 
-template <typename T, class A>
-__device__ void stats_pass(TreeSmem& sm, const T* rb, const T* rs, int V, bool two, const A& ar,
-                           int node, bool gather) {
+template <typename T, class A, bool TWO>
+__device__ __forceinline__ void stats_pass(TreeSmem& sm, const T* rb, const T* rs, int V,
+                                           const A& ar, int node, bool gather) {
   constexpr int E = Elem<T>::E;
   const int tid = threadIdx.x;
-  // Parent's logits at the children's tokens (for the ratios of Alg. 3 init).
-  if (gather && tid < sm.child_count[node]) {
-    const int c = sm.child_list[sm.child_start[node] + tid];
-    const int x = sm.token[c];
-    sm.gzb[c] = Elem<T>::scalar(rb + x);
-    sm.gzs[c] = Elem<T>::scalar(rs + x);
+  // The parent's logits at its children's tokens: loaded now, used after the
+  // reduction (by the same threads), so the row stream does not wait on them.
+  const bool gthread = gather && tid < sm.child_count[node];
+  int gchild = 0;
+  float gb = 0.0f, gs = 0.0f;
+  if (gthread) {
+    gchild = sm.child_list[sm.child_start[node] + tid];
+    const int x = sm.token[gchild];
+    gb = Elem<T>::scalar(rb + x);
+    gs = Elem<T>::scalar(rs + x);
   }
   const Geom g = row_geom(rb, V);
-  Online ob{-INFINITY, 0.0, 0.0}, os{-INFINITY, 0.0, 0.0};
-  if (tid < g.head) {
-    float xb[1] = {Elem<T>::scalar(rb + tid)};
-    online_add(ob, xb, 1, ar);
-    if (two) {
-      float xs[1] = {Elem<T>::scalar(rs + tid)};
-      online_add(os, xs, 1, ar);
+  Online ob = online_init(ar), os = online_init(ar);
+  auto scalar_elem = [&](int i) {
+    float xb[1] = {Elem<T>::scalar(rb + i)};
+    online_raise(ob, xb[0], ar);
+    online_sum(ob, xb, ar);
+    if constexpr (TWO) {
+      float xs[1] = {Elem<T>::scalar(rs + i)};
+      online_raise(os, xs[0], ar);
+      online_sum(os, xs, ar);
     }
-  }
-  const int tail0 = g.head + g.nvec * E;
-  if (tid < g.tail) {
-    float xb[1] = {Elem<T>::scalar(rb + tail0 + tid)};
-    online_add(ob, xb, 1, ar);
-    if (two) {
-      float xs[1] = {Elem<T>::scalar(rs + tail0 + tid)};
-      online_add(os, xs, 1, ar);
-    }
-  }
+  };
+  if (tid < g.head) scalar_elem(tid);
+  if (tid < g.tail) scalar_elem(g.head + g.nvec * E + tid);
   for (int v0 = tid; v0 < g.nvec; v0 += kThreads * kUnroll) {
     uint4 lb[kUnroll], ls[kUnroll];
 #pragma unroll
@@ -320,93 +335,181 @@ __device__ void stats_pass(TreeSmem& sm, const T* rb, const T* rs, int V, bool t
       const int v = v0 + u * kThreads;
       if (v < g.nvec) {
         lb[u] = load16(rb, g.head, v);
-        if (two) ls[u] = load16(rs, g.head, v);
+        if constexpr (TWO) ls[u] = load16(rs, g.head, v);
       }
     }
+    // one rescale per group of kUnroll vectors and row
+    float xb[kUnroll][E], xs[kUnroll][E];
+    float mb = -INFINITY, ms = -INFINITY;
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int v = v0 + u * kThreads;
-      if (v < g.nvec) {
-        float x[E];
-        Elem<T>::unpack(lb[u], x);
-        online_add(ob, x, E, ar);
-        if (two) {
-          Elem<T>::unpack(ls[u], x);
-          online_add(os, x, E, ar);
+      if (v0 + u * kThreads < g.nvec) {
+        Elem<T>::unpack(lb[u], xb[u]);
+        mb = fmaxf(mb, vec_max(xb[u]));
+        if constexpr (TWO) {
+          Elem<T>::unpack(ls[u], xs[u]);
+          ms = fmaxf(ms, vec_max(xs[u]));
         }
       }
     }
+    online_raise(ob, mb, ar);
+    if constexpr (TWO) online_raise(os, ms, ar);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (v0 + u * kThreads < g.nvec) {
+        online_sum(ob, xb[u], ar);
+        if constexpr (TWO) online_sum(os, xs[u], ar);
+      }
+    }
   }
-  finish_online(sm, ob, ar, 0, &sm.res_m[0], &sm.cb[node], &sm.res_s[0]);
-  if (two) finish_online(sm, os, ar, 1, &sm.res_m[1], &sm.cs[node], &sm.res_s[1]);
+  // both rows' maxima in one round, then both rows' sums in one round
+  float Mb = ob.m, Ms = TWO ? os.m : -INFINITY;
+  block_max2(sm, Mb, Ms);
+  const double Cb = ar.frame(Mb);
+  const double Cs = TWO ? ar.frame(Ms) : 0.0;
+  // exact fp64 change of frame; a thread that saw no finite value has s = 0
+  // (or NaN) and a factor 0 unless the whole row has no finite value
+  double Sb = ob.s * exp2(Cb - ob.c);
+  double Ss = TWO ? os.s * exp2(Cs - os.c) : 0.0;
+  block_sum2(sm, Sb, Ss);
+  const bool bad = !(Mb > -INFINITY) || !isfinite(Sb) ||
+                   (TWO && (!(Ms > -INFINITY) || !isfinite(Ss)));
   if (tid == 0) {
-    bool bad = !(sm.res_m[0] > -INFINITY) || !isfinite(sm.res_s[0]);
-    sm.lsb[node] = log2(sm.res_s[0]);
-    if (two) {
-      bad = bad || !(sm.res_m[1] > -INFINITY) || !isfinite(sm.res_s[1]);
-      sm.lss[node] = log2(sm.res_s[1]);
+    sm.cb[node] = Cb;
+    sm.invsb[node] = 1.0 / Sb;
+    if constexpr (TWO) {
+      sm.cs[node] = Cs;
+      sm.invss[node] = 1.0 / Ss;
     }
     sm.res_bad = bad ? 1 : 0;
+    sm.gather_bad = 0;
   }
   __syncthreads();
-  if (gather && tid < sm.child_count[node]) {
-    const int c = sm.child_list[sm.child_start[node] + tid];
-    if (sm.gzs[c] == -INFINITY) sm.res_bad = 1;    // token the draft cannot produce
+  // Children's original ratios r0 = p(x)/q(x) and draft terms, one thread each.
+  if (gthread && !bad) {
+    const double kd = ar.kd();
+    const double lp = fma(static_cast<double>(gb), kd, Cb) - log2(Sb);
+    const double lq = fma(static_cast<double>(gs), kd, Cs) - log2(Ss);
+    sm.r0[gchild] = exp2(lp - lq);
+    sm.et[gchild] = ar.ex(gs, Cs);
+    if (gs == -INFINITY) sm.gather_bad = 1;     // token the draft cannot produce
   }
   __syncthreads();
+  if (tid == 0 && sm.gather_bad) sm.res_bad = 1;
 }
 
 // ---------------------------------------------------------------------------
-// Residual terms [ap * tb - bp * ts]_+ with tb, ts the target and draft terms
-// of a row (two == false: target only, weight ap * tb).
+// Residual weights max(ap * tb - bp * ts, 0), tb and ts the target and draft
+// terms of an element (TWO == false: target only, weight ap * tb). With SD the
+// draft terms are also summed, exactly in fp64.
 // ---------------------------------------------------------------------------
 
-template <class A>
-struct TermCtx {
-  A ar;
-  double cb, cs;
-  double ap, bp;
-  bool two;
+struct TermParams {
+  double cb, cs;   // frames of the target and draft rows
+  double ap, bp;   // multipliers of the target and draft terms
 };
 
-// One element: returns the residual weight and adds the draft term to *sd.
-template <class A>
-__device__ inline double term(const TermCtx<A>& t, float zb, float zs, double* sd) {
-  const double eb = t.ar.ex(zb, t.cb);
-  if (!t.two) return t.ap * eb;
-  const double es = t.ar.ex(zs, t.cs);
-  *sd += es;
-  return fmax(fma(eb, t.ap, -es * t.bp), 0.0);
-}
+template <class A, bool TWO, bool SD> struct Terms;
 
-template <typename T, class A>
-__device__ inline double vec_terms(const TermCtx<A>& t, const uint4& vb, const uint4& vs,
-                                   double* sd) {
+// Fast path: fp32 per element; the weights of one vector are summed in fp32
+// and the vector sums in fp64.
+template <bool TWO, bool SD> struct Terms<FastArith, TWO, SD> {
+  float k, cb, cs, ap, bp;
+  __device__ Terms(const FastArith& ar, const TermParams& p)
+      : k(ar.k), cb(static_cast<float>(p.cb)), cs(static_cast<float>(p.cs)),
+        ap(static_cast<float>(p.ap)), bp(static_cast<float>(p.bp)) {}
+  template <int N>
+  __device__ __forceinline__ void weights(const float (&zb)[N], const float (&zs)[N],
+                                          float (&w)[N], double& sd) const {
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      const float eb = fast_exp2(fmaf(zb[e], k, cb));
+      if constexpr (TWO) {
+        const float es = fast_exp2(fmaf(zs[e], k, cs));
+        if constexpr (SD) sd += static_cast<double>(es);
+        w[e] = fmaxf(fmaf(eb, ap, -es * bp), 0.0f);
+      } else {
+        w[e] = eb * ap;
+      }
+    }
+  }
+  template <int N>
+  __device__ __forceinline__ double sum(const float (&zb)[N], const float (&zs)[N],
+                                        double& sd) const {
+    float w[N];
+    weights(zb, zs, w, sd);
+    float acc = 0.0f;
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc += w[e];
+    return static_cast<double>(acc);
+  }
+};
+
+// Precise path: fp64 throughout.
+template <bool TWO, bool SD> struct Terms<PreciseArith, TWO, SD> {
+  double k, cb, cs, ap, bp;
+  __device__ Terms(const PreciseArith& ar, const TermParams& p)
+      : k(ar.k), cb(p.cb), cs(p.cs), ap(p.ap), bp(p.bp) {}
+  template <int N>
+  __device__ __forceinline__ void weights(const float (&zb)[N], const float (&zs)[N],
+                                          double (&w)[N], double& sd) const {
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      const double eb = exp2(fma(static_cast<double>(zb[e]), k, cb));
+      if constexpr (TWO) {
+        const double es = exp2(fma(static_cast<double>(zs[e]), k, cs));
+        if constexpr (SD) sd += es;
+        w[e] = fmax(fma(eb, ap, -es * bp), 0.0);
+      } else {
+        w[e] = eb * ap;
+      }
+    }
+  }
+  template <int N>
+  __device__ __forceinline__ double sum(const float (&zb)[N], const float (&zs)[N],
+                                        double& sd) const {
+    double w[N];
+    weights(zb, zs, w, sd);
+    double acc = 0.0;
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc += w[e];
+    return acc;
+  }
+};
+
+template <typename T, class TM, bool TWO>
+__device__ __forceinline__ double vec_sum(const TM& tm, const uint4& vb, const uint4& vs,
+                                          double& sd) {
   constexpr int E = Elem<T>::E;
   float xb[E], xs[E];
   Elem<T>::unpack(vb, xb);
-  if (t.two) Elem<T>::unpack(vs, xs);
-  double acc = 0.0;
+  if constexpr (TWO) Elem<T>::unpack(vs, xs);
+  else {
 #pragma unroll
-  for (int e = 0; e < E; ++e) acc += term(t, xb[e], t.two ? xs[e] : 0.0f, sd);
-  return acc;
+    for (int e = 0; e < E; ++e) xs[e] = 0.0f;
+  }
+  return tm.sum(xb, xs, sd);
 }
 
-template <typename T, class A>
-__device__ inline double scalar_term(const TermCtx<A>& t, const T* rb, const T* rs, int i,
-                                     double* sd) {
-  return term(t, Elem<T>::scalar(rb + i), t.two ? Elem<T>::scalar(rs + i) : 0.0f, sd);
+template <typename T, class TM, bool TWO>
+__device__ __forceinline__ double scalar_weight(const TM& tm, const T* rb, const T* rs, int i,
+                                                double& sd) {
+  float xb[1] = {Elem<T>::scalar(rb + i)};
+  float xs[1] = {TWO ? Elem<T>::scalar(rs + i) : 0.0f};
+  return tm.sum(xb, xs, sd);
 }
 
-// S = sum of the residual weights (Eq. e1, e3) and the sum of the draft terms.
-template <typename T, class A>
-__device__ void s_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const TermCtx<A>& t) {
+// S = sum of the residual weights (Eq. e1, e3); with SD also the draft-term sum.
+template <typename T, class A, bool SD>
+__device__ __forceinline__ void s_pass(TreeSmem& sm, const T* rb, const T* rs, int V,
+                                       const A& ar, const TermParams& p) {
+  const Terms<A, true, SD> tm(ar, p);
   const int tid = threadIdx.x;
   const Geom g = row_geom(rb, V);
   double acc = 0.0, sd = 0.0;
-  if (tid < g.head) acc += scalar_term(t, rb, rs, tid, &sd);
+  if (tid < g.head) acc += scalar_weight<T, decltype(tm), true>(tm, rb, rs, tid, sd);
   const int tail0 = g.head + g.nvec * Elem<T>::E;
-  if (tid < g.tail) acc += scalar_term(t, rb, rs, tail0 + tid, &sd);
+  if (tid < g.tail) acc += scalar_weight<T, decltype(tm), true>(tm, rb, rs, tail0 + tid, sd);
   for (int v0 = tid; v0 < g.nvec; v0 += kThreads * kUnroll) {
     uint4 lb[kUnroll], ls[kUnroll];
 #pragma unroll
@@ -420,14 +523,13 @@ __device__ void s_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const Term
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int v = v0 + u * kThreads;
-      if (v < g.nvec) acc += vec_terms<T>(t, lb[u], ls[u], &sd);
+      if (v < g.nvec) acc += vec_sum<T, decltype(tm), true>(tm, lb[u], ls[u], sd);
     }
   }
-  const double S = block_sum(sm, acc, 0);
-  const double SD = block_sum(sm, sd, 1);
+  block_sum2(sm, acc, sd);
   if (tid == 0) {
-    sm.res_S = S;
-    sm.res_sd = SD;
+    sm.res_S = acc;
+    if constexpr (SD) sm.res_sd = sd;
   }
   __syncthreads();
 }
@@ -438,32 +540,46 @@ __device__ void s_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const Term
 // wavefront and iteration), then tail elements.
 // ---------------------------------------------------------------------------
 
-template <typename T, class A>
-__device__ void sample_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const TermCtx<A>& t,
-                            float u) {
+template <typename T, class A, bool TWO>
+__device__ __forceinline__ void sample_pass(TreeSmem& sm, const T* rb, const T* rs, int V,
+                                            const A& ar, const TermParams& p, float u) {
   constexpr int E = Elem<T>::E;
+  constexpr int kU = 2;            // iterations (vectors per lane) in flight
+  const Terms<A, TWO, false> tm(ar, p);
+  using TM = Terms<A, TWO, false>;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const Geom g = row_geom(rb, V);
   const int tail0 = g.head + g.nvec * E;
   const int nblocks = (g.nvec + 63) / 64;
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  const int iters = (g.nvec + kThreads - 1) / kThreads;
   double unused = 0.0;
-  for (int it = 0; it * kThreads < g.nvec; ++it) {
-    const int v = it * kThreads + tid;
-    double l = 0.0;
-    if (v < g.nvec) {
-      const uint4 vb = load16(rb, g.head, v);
-      const uint4 vs = t.two ? load16(rs, g.head, v) : zero4;
-      l = vec_terms<T>(t, vb, vs, &unused);
+  for (int it0 = 0; it0 < iters; it0 += kU) {
+    uint4 lb[kU], ls[kU];
+#pragma unroll
+    for (int q = 0; q < kU; ++q) {
+      const int v = (it0 + q) * kThreads + tid;
+      lb[q] = make_uint4(0, 0, 0, 0);
+      ls[q] = make_uint4(0, 0, 0, 0);
+      if (v < g.nvec) {
+        lb[q] = load16(rb, g.head, v);
+        if constexpr (TWO) ls[q] = load16(rs, g.head, v);
+      }
     }
-    l = wave_sum(l);
-    const int blk = it * kWaves + wave;
-    if (lane == 0 && blk < nblocks) sm.blocks[blk] = l;
+#pragma unroll
+    for (int q = 0; q < kU; ++q) {
+      if (it0 + q < iters) {
+        const int v = (it0 + q) * kThreads + tid;
+        double l = v < g.nvec ? vec_sum<T, TM, TWO>(tm, lb[q], ls[q], unused) : 0.0;
+        l = wave_sum(l);
+        const int blk = (it0 + q) * kWaves + wave;
+        if (lane == 0 && blk < nblocks) sm.blocks[blk] = l;
+      }
+    }
   }
   if (tid == 0) {
     double h = 0.0, tl = 0.0;
-    for (int i = 0; i < g.head; ++i) h += scalar_term(t, rb, rs, i, &unused);
-    for (int i = tail0; i < V; ++i) tl += scalar_term(t, rb, rs, i, &unused);
+    for (int i = 0; i < g.head; ++i) h += scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
+    for (int i = tail0; i < V; ++i) tl += scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
     sm.res_head = h;
     sm.res_tail = tl;
   }
@@ -482,7 +598,7 @@ __device__ void sample_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const
     } else {
       double C = 0.0;
       for (int i = 0; i < g.head && y < 0; ++i) {
-        const double w = scalar_term(t, rb, rs, i, &unused);
+        const double w = scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
         if (target < C + w) y = i;
         C += w;
       }
@@ -499,7 +615,7 @@ __device__ void sample_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const
       if (y < 0 && found_block < 0) {
         int last = -1;
         for (int i = tail0; i < V; ++i) {
-          const double w = scalar_term(t, rb, rs, i, &unused);
+          const double w = scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
           if (w > 0.0) last = i;
           if (target < C + w) { y = i; break; }
           C += w;
@@ -521,15 +637,24 @@ __device__ void sample_pass(TreeSmem& sm, const T* rb, const T* rs, int V, const
     for (int e = 0; e < E; ++e) wd[e] = 0.0;
     if (v < g.nvec) {
       const uint4 vb = load16(rb, g.head, v);
-      const uint4 vs = t.two ? load16(rs, g.head, v) : zero4;
+      uint4 vs = make_uint4(0, 0, 0, 0);
+      if constexpr (TWO) vs = load16(rs, g.head, v);
       float xb[E], xs[E];
       Elem<T>::unpack(vb, xb);
-      if (t.two) Elem<T>::unpack(vs, xs);
+      Elem<T>::unpack(vs, xs);
+      // the same per-element weights (and vector sum) as in the pass above
+      if constexpr (A::kPrecise) {
+        double w[E];
+        tm.weights(xb, xs, w, unused);
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        wd[e] = term(t, xb[e], t.two ? xs[e] : 0.0f, &unused);
-        l += wd[e];
+        for (int e = 0; e < E; ++e) wd[e] = w[e];
+      } else {
+        float w[E];
+        tm.weights(xb, xs, w, unused);
+#pragma unroll
+        for (int e = 0; e < E; ++e) wd[e] = static_cast<double>(w[e]);
       }
+      l = vec_sum<T, TM, TWO>(tm, vb, vs, unused);
     }
     // inclusive scan over lanes
     double incl = l;
@@ -592,41 +717,28 @@ struct Params {
   double k64;     // log2(e) / T (precise element path)
 };
 
-// log2 of the target / draft probability of child c's token at its parent j,
-// in the same frame and scale as the row sums.
-template <class A>
-__device__ inline double log2_p(const TreeSmem& sm, const A& ar, int j, int c) {
-  return fma(static_cast<double>(sm.gzb[c]), ar.kd(), sm.cb[j]) - sm.lsb[j];
-}
-template <class A>
-__device__ inline double log2_q(const TreeSmem& sm, const A& ar, int j, int c) {
-  return fma(static_cast<double>(sm.gzs[c]), ar.kd(), sm.cs[j]) - sm.lss[j];
-}
-
 // Chain rate of child c given its parent j's current state:
-// min(pi_j * b_j(x) / s_j(x), 1) with b/s = [A r - B]_+ * (remaining draft mass).
-template <class A>
-__device__ inline double child_rate(const TreeSmem& sm, const A& ar, int mode, int j, int c) {
+// min(pi_j * b_j(x)/s_j(x), 1) with b/s = [A r - B]_+ * (remaining draft mass).
+__device__ inline double child_rate(const TreeSmem& sm, int mode, int j, int c) {
   if (sm.pi[j] == 0.0) return 0.0;
-  const double r = exp2(log2_p(sm, ar, j, c) - log2_q(sm, ar, j, c));
-  double v = fmax(sm.A[j] * r - sm.B[j], 0.0);
+  double v = fmax(sm.A[j] * sm.r0[c] - sm.B[j], 0.0);
   if (mode == TV_SIBLINGS_WITHOUT_REPLACEMENT) v *= sm.rem[j];
   if (v == 0.0) return 0.0;
   return fmin(sm.pi[j] * v, 1.0);
 }
 
-// After a pass at j that rejected child `last`: draft mass left once every
-// rejected child's token is removed (Eq. e2 applied to all of them), from the
-// pass's own draft-term sum minus those tokens' terms, recomputed identically.
-template <class A>
-__device__ inline void update_remaining_mass(TreeSmem& sm, const A& ar, int j) {
-  const double total = sm.res_sd;
+// After a pass at j that rejected a child: draft mass left once every rejected
+// child's token is removed (Eq. e2 applied to all of them), from the pass's own
+// draft-term sum minus those tokens' terms, computed the same way.
+__device__ inline void update_remaining_mass(TreeSmem& sm, int j) {
+  if (sm.cmd_sd) {
+    sm.sdsum[j] = sm.res_sd;
+    sm.flags[j] |= kFlagSd;
+  }
+  const double total = sm.sdsum[j];
   double removed = 0.0;
   const int s0 = sm.child_start[j];
-  for (int r = 0; r < sm.next_child[j]; ++r) {
-    const int c = sm.child_list[s0 + r];
-    removed += ar.ex(sm.gzs[c], sm.cs[j]);
-  }
+  for (int r = 0; r < sm.next_child[j]; ++r) removed += sm.et[sm.child_list[s0 + r]];
   sm.rem[j] = (total - removed) / total;
 }
 
@@ -637,12 +749,13 @@ __device__ inline void issue_stats(TreeSmem& sm, int node, bool two, bool gather
   sm.cmd_gather = gather ? 1 : 0;
 }
 
-__device__ inline void issue_spass(TreeSmem& sm, int node, double alpha, double beta) {
+__device__ inline void issue_spass(TreeSmem& sm, int node, double alpha, double beta, bool wo) {
   sm.cmd = kCmdSPass;
   sm.cmd_node = node;
   sm.cmd_two_rows = 1;
-  sm.cmd_ap = alpha * exp2(-sm.lsb[node]);
-  sm.cmd_bp = beta * exp2(-sm.lss[node]);
+  sm.cmd_sd = (wo && !(sm.flags[node] & kFlagSd)) ? 1 : 0;
+  sm.cmd_ap = alpha * sm.invsb[node];
+  sm.cmd_bp = beta * sm.invss[node];
   sm.cmd_cb = sm.cb[node];
   sm.cmd_cs = sm.cs[node];
 }
@@ -658,8 +771,8 @@ __device__ inline void issue_sample(TreeSmem& sm, int node, bool leaf) {
     sm.cmd_cs = 0.0;
   } else {
     sm.cmd_two_rows = 1;
-    sm.cmd_ap = sm.A[node] * exp2(-sm.lsb[node]);
-    sm.cmd_bp = sm.B[node] * exp2(-sm.lss[node]);
+    sm.cmd_ap = sm.A[node] * sm.invsb[node];
+    sm.cmd_bp = sm.B[node] * sm.invss[node];
     sm.cmd_cs = sm.cs[node];
   }
 }
@@ -678,7 +791,7 @@ __device__ inline void init_node_state(TreeSmem& sm, int c, double pi) {
 
 // Runs until the next vocabulary pass is needed (or the tree is done).
 template <class A>
-__device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
+__device__ __attribute__((noinline)) void advance(TreeSmem& sm, const Params& P, const A& ar) {
   if (sm.cmd == kCmdStats) {
     const int j = sm.cmd_node;
     if (sm.res_bad) { fail(sm, TV_TREE_NONFINITE); return; }
@@ -702,8 +815,7 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
         for (int i = 1; i < P.num_nodes; ++i) {
           const int j = sm.parent[i];
           if (sm.pini[j] == 0.0) { sm.pini[i] = 0.0; continue; }
-          const double r = exp2(log2_p(sm, ar, j, i) - log2_q(sm, ar, j, i));
-          sm.pini[i] = fmin(sm.pini[j] * r, 1.0);
+          sm.pini[i] = fmin(sm.pini[j] * sm.r0[i], 1.0);
         }
         sm.phase = sm.algo == static_cast<int>(tv::Algo::kTraversal) ? kPhDescend : kPhTlVisit;
         continue;
@@ -720,7 +832,7 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
             if (!(sm.flags[j] & kFlagStats)) { issue_stats(sm, j, true, true); return; }
           }
           const int c = sm.child_list[sm.child_start[j] + sm.next_child[j]];
-          init_node_state(sm, c, child_rate(sm, ar, P.mode, j, c));
+          init_node_state(sm, c, child_rate(sm, P.mode, j, c));
           sm.cur = c;
           continue;
         }
@@ -760,7 +872,7 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
         sm.beta = sm.pi[j] * sm.B[j] + cc;
         sm.rejected = l;
         sm.phase = kPhAfterSPass;
-        issue_spass(sm, j, sm.alpha, sm.beta);
+        issue_spass(sm, j, sm.alpha, sm.beta, wo);
         return;
       }
       case kPhAfterSPass: {                 // Eq. (e1), (e2), (e3) at the parent
@@ -769,8 +881,9 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
         const double S = sm.res_S;
         ++sm.resid_passes;
         if (S > 0.0) {
-          sm.A[j] = sm.alpha / S;
-          sm.B[j] = sm.beta / S;
+          const double inv = 1.0 / S;
+          sm.A[j] = sm.alpha * inv;
+          sm.B[j] = sm.beta * inv;
           sm.pi[j] = S / (S + (1.0 - sm.pi[j]));
         } else if (j == 0) {
           fail(sm, TV_TREE_DEGENERATE);
@@ -778,7 +891,7 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
         } else {
           sm.pi[j] = 0.0;
         }
-        if (wo) update_remaining_mass(sm, ar, j);
+        if (wo) update_remaining_mass(sm, j);
         sm.cur = j;
         sm.phase = kPhDescend;
         continue;
@@ -804,7 +917,7 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
           continue;
         }
         const int c = sm.child_list[sm.child_start[j] + sm.next_child[j]];
-        const double th = child_rate(sm, ar, P.mode, j, c);
+        const double th = child_rate(sm, P.mode, j, c);
         sm.theta[c] = static_cast<float>(th);
         ++sm.tests;
         if (static_cast<double>(sm.u[c]) < th) {
@@ -820,7 +933,7 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
         sm.beta = sm.B[j] + cc;
         sm.rejected = c;
         sm.phase = kPhTlAfterSPass;
-        issue_spass(sm, j, sm.alpha, sm.beta);
+        issue_spass(sm, j, sm.alpha, sm.beta, wo);
         return;
       }
       case kPhTlAfterSPass: {               // Algorithm 2 rejection branch
@@ -829,9 +942,10 @@ __device__ void advance(TreeSmem& sm, const Params& P, const A& ar) {
         const double S = sm.res_S;
         ++sm.resid_passes;
         if (!(S > 0.0)) { fail(sm, TV_TREE_DEGENERATE); return; }
-        sm.A[j] = sm.alpha / S;
-        sm.B[j] = sm.beta / S;
-        if (wo) update_remaining_mass(sm, ar, j);
+        const double inv = 1.0 / S;
+        sm.A[j] = sm.alpha * inv;
+        sm.B[j] = sm.beta * inv;
+        if (wo) update_remaining_mass(sm, j);
         sm.phase = kPhTlVisit;
         continue;
       }
@@ -957,6 +1071,7 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
       init_node_state(sm, 0, 1.0);
       sm.res_y = -1;
       sm.cmd = -1;
+      sm.cmd_sd = 0;
       if (P.p_init && algo == static_cast<int>(tv::Algo::kTraversal)) sm.phase = kPhPinit;
       else if (algo == static_cast<int>(tv::Algo::kTraversal)) sm.phase = kPhDescend;
       else sm.phase = kPhTlVisit;
@@ -970,12 +1085,18 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
       const T* rb = zb + static_cast<size_t>(node) * V;
       const T* rs = zs + static_cast<size_t>(node) * V;
       if (cmd == kCmdStats) {
-        stats_pass<T>(sm, rb, rs, V, sm.cmd_two_rows != 0, ar, node, sm.cmd_gather != 0);
+        if (sm.cmd_two_rows) stats_pass<T, A, true>(sm, rb, rs, V, ar, node, sm.cmd_gather != 0);
+        else stats_pass<T, A, false>(sm, rb, rs, V, ar, node, false);
       } else {
-        const TermCtx<A> t{ar, sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp,
-                           sm.cmd_two_rows != 0};
-        if (cmd == kCmdSPass) s_pass<T>(sm, rb, rs, V, t);
-        else sample_pass<T>(sm, rb, rs, V, t, sm.u[0]);
+        const TermParams tp{sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp};
+        if (cmd == kCmdSPass) {
+          if (sm.cmd_sd) s_pass<T, A, true>(sm, rb, rs, V, ar, tp);
+          else s_pass<T, A, false>(sm, rb, rs, V, ar, tp);
+        } else if (sm.cmd_two_rows) {
+          sample_pass<T, A, true>(sm, rb, rs, V, ar, tp, sm.u[0]);
+        } else {
+          sample_pass<T, A, false>(sm, rb, rs, V, ar, tp, sm.u[0]);
+        }
       }
       if (tid == 0) advance(sm, P, ar);
       __syncthreads();

@@ -43,6 +43,7 @@ def test_constants_match_header():
 
     assert eval(define("TV_MAX_NODES")) == tv.TV_MAX_NODES
     assert eval(define("TV_MAX_VOCAB")) == tv.TV_MAX_VOCAB
+    assert eval(define("TV_MAX_VOCAB_F32")) == tv.TV_MAX_VOCAB_F32
     assert eval(define("TV_NUM_COUNTERS")) == tv.TV_NUM_COUNTERS
     for name in ["TV_OK", "TV_ERR_INVALID_ARG", "TV_ERR_UNSUPPORTED", "TV_ERR_WORKSPACE",
                  "TV_ERR_HIP", "TV_DTYPE_BF16", "TV_DTYPE_F32", "TV_SIBLINGS_WITHOUT_REPLACEMENT",
@@ -92,6 +93,7 @@ def call(fn="tv_verify", **kw):
     (dict(temperature=1e4), tv.TV_ERR_UNSUPPORTED),
     (dict(num_nodes=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
     (dict(vocab=tv.TV_MAX_VOCAB + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(dtype=tv.TV_DTYPE_F32, vocab=tv.TV_MAX_VOCAB_F32 + 1), tv.TV_ERR_UNSUPPORTED),
     (dict(parents=None), tv.TV_ERR_INVALID_ARG),
     (dict(tokens=None), tv.TV_ERR_INVALID_ARG),
     (dict(target_logits=None), tv.TV_ERR_INVALID_ARG),
