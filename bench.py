@@ -157,6 +157,8 @@ def main():
     elem = 2
     stream = torch.cuda.current_stream(dev)
 
+    workspace, _ = tv.workspace_tensor(B, n1, V, dev)
+
     def one_step(step, tokenlevel=False):
         batch = W.make_batch(CFG, step=step, device=dev, mode=mode, seed=1)
         torch.cuda.synchronize()
@@ -166,7 +168,7 @@ def main():
         out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"],
                               batch["draft"], batch["temperature"], batch["uniforms"], mode,
                               tokenlevel=tokenlevel, want_nodes=False, want_counters=True,
-                              stream=stream.cuda_stream)
+                              stream=stream.cuda_stream, workspace=workspace)
         ev1.record(stream)
         torch.cuda.synchronize()
         return ev0.elapsed_time(ev1), batch, out
@@ -222,7 +224,8 @@ def main():
             else cfg.name + " (siblings i.i.d.)",
             "batch": B, "rows_per_tree": n1, "vocab": V, "input_dtype": "bf16",
             "temperature": cfg.temperature, "mode": args.mode + "_replacement",
-            "parallelism": "single GPU, one workgroup per tree",
+            "parallelism": "single GPU; one owner workgroup per tree, vocabulary passes "
+                           "shared by all workgroups in 2048-vector segments",
         },
         "ms_p50": srt[len(srt) // 2],
         "ms_p90": srt[min(len(srt) - 1, int(0.9 * len(srt)))],

@@ -25,11 +25,21 @@
  *     order (the smallest y with u * W < C(y), C the running sum, W its total).
  *
  * Memory and streams. Every pointer is a device pointer. The caller owns all
- * buffers; the library allocates nothing, keeps no state between calls and
- * never synchronises the host: work is enqueued on `stream` and the call
- * returns. Inputs are read-only. Outputs are written for every tree, including
- * trees whose status is not TV_TREE_OK (they get -1 sentinels). Calls that
- * write the same output buffers must be ordered by the caller.
+ * buffers, including a device workspace of tv_workspace_size() bytes that the
+ * call uses as scratch (work queue, counters and partial sums; its contents
+ * need no initialisation and are meaningless afterwards). The library
+ * allocates nothing, keeps no state between calls and never synchronises the
+ * host: work is enqueued on `stream` and the call returns. Inputs are
+ * read-only. Outputs are written for every tree, including trees whose status
+ * is not TV_TREE_OK (they get -1 sentinels). Calls that write the same output
+ * buffers or share a workspace must be ordered by the caller.
+ *
+ * Execution. One call launches a persistent grid of at most as many
+ * workgroups as the device can hold at once; idle workgroups wait for work in
+ * the other trees of the batch. Calls on concurrent streams of one device can
+ * therefore hold each other's workgroups back; every wait is bounded, and a
+ * call that makes no progress for 4 seconds gives up and reports
+ * TV_TREE_ABORTED for the trees it did not finish.
  *
  * Errors. Argument problems the host can see (null pointers, sizes, enums,
  * temperature, misaligned pointers) return a tv_status_t other than TV_OK and
@@ -53,7 +63,8 @@ typedef enum tv_status {
   TV_ERR_INVALID_ARG = 1,  /* null pointer, negative size, unknown enum, T <= 0 or not finite */
   TV_ERR_UNSUPPORTED = 2,  /* size or temperature beyond the limits below, or target and draft
                               pointers whose addresses differ modulo 16 bytes */
-  TV_ERR_WORKSPACE = 3,    /* workspace smaller than tv_workspace_size() or misaligned */
+  TV_ERR_WORKSPACE = 3,    /* workspace NULL, smaller than tv_workspace_size() or not
+                              256-byte aligned */
   TV_ERR_HIP = 4           /* the kernel launch failed (hipGetLastError) */
 } tv_status_t;
 
@@ -85,8 +96,10 @@ enum {
   TV_TREE_DUP_SIBLING = 3, /* two siblings share a token in WITHOUT_REPLACEMENT mode */
   TV_TREE_NONFINITE = 4,   /* a row the verifier read holds NaN or +inf or no finite value,
                               or a drafted token has draft logit -inf */
-  TV_TREE_DEGENERATE = 5   /* a residual distribution the algorithm samples from has zero
+  TV_TREE_DEGENERATE = 5,  /* a residual distribution the algorithm samples from has zero
                               mass in floating point (impossible in exact arithmetic) */
+  TV_TREE_ABORTED = 6      /* not verified: the call gave up after its wait limit (see
+                              Execution above) */
 };
 
 /* Values written to node_state[b][i]. */
@@ -102,6 +115,7 @@ enum {
 };
 
 /* Limits of this implementation. */
+#define TV_MAX_BATCH (1 << 20)     /* trees per call */
 #define TV_MAX_NODES 1024          /* num_nodes = N + 1 (root included) */
 #define TV_MAX_VOCAB (1 << 20)          /* bf16 logits */
 #define TV_MAX_VOCAB_F32 (1 << 19)      /* fp32 logits */
@@ -111,8 +125,9 @@ enum {
 
 /*
  * Bytes of device workspace tv_verify / tv_verify_tokenlevel need for these
- * sizes (0 means none; pass workspace = NULL then). Returns 0 for invalid
- * sizes too.
+ * sizes (valid for either dtype; at most about 65 MiB, about 16 MiB for 256
+ * trees at V = 128256). Returns 0 for invalid sizes (batch < 1, vocab < 2 or
+ * beyond the limits below); a batch of 0 needs no workspace.
  */
 size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab);
 
@@ -148,7 +163,6 @@ size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab);
  *                  [2] 1 if the accepted node has no children (its target row is read for Y),
  *                  [3] nodes tested against their uniform
  *   workspace      device buffer of at least tv_workspace_size() bytes, 256-byte aligned
- *                  (NULL if that size is 0)
  *   stream         HIP stream the work is enqueued on (NULL: the default stream)
  * Returns a tv_status_t.
  */

@@ -12,10 +12,10 @@ from ._lib import (  # noqa: F401
     TV_DTYPE_BF16, TV_DTYPE_F32,
     TV_SIBLINGS_WITHOUT_REPLACEMENT, TV_SIBLINGS_WITH_REPLACEMENT,
     TV_TREE_OK, TV_TREE_BAD_PARENT, TV_TREE_BAD_TOKEN, TV_TREE_DUP_SIBLING,
-    TV_TREE_NONFINITE, TV_TREE_DEGENERATE,
+    TV_TREE_NONFINITE, TV_TREE_DEGENERATE, TV_TREE_ABORTED,
     TV_NODE_UNTESTED, TV_NODE_ACCEPTED, TV_NODE_REJECTED, TV_NODE_PRUNED,
-    TV_MAX_NODES, TV_MAX_VOCAB, TV_MAX_VOCAB_F32, TV_NUM_COUNTERS,
+    TV_MAX_BATCH, TV_MAX_NODES, TV_MAX_VOCAB, TV_MAX_VOCAB_F32, TV_NUM_COUNTERS,
     LIB_PATH, TvError, load_library,
     tv_workspace_size, tv_verify, tv_verify_tokenlevel, tv_status_string,
-    VerifyOutputs, verify_batch,
+    VerifyOutputs, verify_batch, workspace_tensor,
 )

@@ -12,8 +12,9 @@ TV_OK, TV_ERR_INVALID_ARG, TV_ERR_UNSUPPORTED, TV_ERR_WORKSPACE, TV_ERR_HIP = ra
 TV_DTYPE_BF16, TV_DTYPE_F32 = 0, 1
 TV_SIBLINGS_WITHOUT_REPLACEMENT, TV_SIBLINGS_WITH_REPLACEMENT = 0, 1
 (TV_TREE_OK, TV_TREE_BAD_PARENT, TV_TREE_BAD_TOKEN, TV_TREE_DUP_SIBLING, TV_TREE_NONFINITE,
- TV_TREE_DEGENERATE) = range(6)
+ TV_TREE_DEGENERATE, TV_TREE_ABORTED) = range(7)
 TV_NODE_UNTESTED, TV_NODE_ACCEPTED, TV_NODE_REJECTED, TV_NODE_PRUNED = range(4)
+TV_MAX_BATCH = 1 << 20
 TV_MAX_NODES = 1024
 TV_MAX_VOCAB = 1 << 20
 TV_MAX_VOCAB_F32 = 1 << 19
@@ -117,6 +118,14 @@ def tv_verify_tokenlevel(batch, num_nodes, vocab, parents, tokens, target_logits
                  workspace, workspace_bytes, stream)
 
 
+def workspace_tensor(batch: int, num_nodes: int, vocab: int, device):
+    """A device buffer of tv_workspace_size() bytes (torch allocations are
+    256-byte aligned)."""
+    import torch
+    n = tv_workspace_size(batch, num_nodes, vocab)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device), n
+
+
 @dataclass
 class VerifyOutputs:
     accept_len: object
@@ -131,9 +140,11 @@ class VerifyOutputs:
 
 def verify_batch(parents, tokens, target_logits, draft_logits, temperature, uniforms, mode,
                  tokenlevel=False, want_nodes=True, want_p_init=False, want_counters=True,
-                 out: VerifyOutputs | None = None, stream=None) -> VerifyOutputs:
-    """Allocate outputs (torch, same device) unless given, check shapes, call the
-    C entry point on the current stream and raise on a non-OK return."""
+                 out: VerifyOutputs | None = None, stream=None,
+                 workspace=None) -> VerifyOutputs:
+    """Allocate outputs and the workspace (torch, same device) unless given,
+    check shapes, call the C entry point on the current stream and raise on a
+    non-OK return."""
     import torch
     B, n1 = parents.shape
     V = target_logits.shape[-1]
@@ -165,10 +176,15 @@ def verify_batch(parents, tokens, target_logits, draft_logits, temperature, unif
             counters=torch.empty((B, TV_NUM_COUNTERS), **i32) if want_counters else None)
     if stream is None:
         stream = torch.cuda.current_stream(dev).cuda_stream if dev.type == "cuda" else None
+    if workspace is None:
+        workspace, ws_bytes = workspace_tensor(B, n1, V, dev)
+    else:
+        ws_bytes = workspace.numel() * workspace.element_size()
     fn = tv_verify_tokenlevel if tokenlevel else tv_verify
     st = fn(B, n1, V, parents, tokens, target_logits, draft_logits, dtype, temperature,
             uniforms, mode, out.accept_len, out.accepted_node, out.bonus_token, out.status,
-            out.node_state, out.node_theta, out.p_init, out.counters, None, 0, stream)
+            out.node_state, out.node_theta, out.p_init, out.counters, workspace, ws_bytes,
+            stream)
     if st != TV_OK:
         raise TvError(st, fn.__name__)
     return out

@@ -11,8 +11,6 @@
 namespace tv {
 
 int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
-  (void)workspace;
-  (void)workspace_bytes;
   if (a.batch < 0 || a.num_nodes < 1 || a.vocab < 2) return TV_ERR_INVALID_ARG;
   if (a.dtype != TV_DTYPE_BF16 && a.dtype != TV_DTYPE_F32) return TV_ERR_INVALID_ARG;
   if (a.mode != TV_SIBLINGS_WITHOUT_REPLACEMENT && a.mode != TV_SIBLINGS_WITH_REPLACEMENT)
@@ -20,7 +18,8 @@ int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
   if (!(a.temperature > 0.0f) || !isfinite(a.temperature)) return TV_ERR_INVALID_ARG;
   if (a.temperature < TV_MIN_TEMPERATURE || a.temperature > TV_MAX_TEMPERATURE)
     return TV_ERR_UNSUPPORTED;
-  if (a.num_nodes > TV_MAX_NODES || a.vocab > TV_MAX_VOCAB) return TV_ERR_UNSUPPORTED;
+  if (a.batch > TV_MAX_BATCH || a.num_nodes > TV_MAX_NODES || a.vocab > TV_MAX_VOCAB)
+    return TV_ERR_UNSUPPORTED;
   if (a.dtype == TV_DTYPE_F32 && a.vocab > TV_MAX_VOCAB_F32) return TV_ERR_UNSUPPORTED;
   if (a.batch == 0) return TV_OK;
   if (!a.parents || !a.tokens || !a.target || !a.draft || !a.uniforms || !a.accept_len ||
@@ -35,6 +34,9 @@ int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
                             a.bonus_token, a.status, a.node_theta, a.p_init, a.counters};
   for (const void* p : int_ptrs)
     if (reinterpret_cast<uintptr_t>(p) % 4) return TV_ERR_INVALID_ARG;
+  if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 256 ||
+      workspace_bytes < workspace_layout(a.batch, a.vocab).bytes)
+    return TV_ERR_WORKSPACE;
   return TV_OK;
 }
 
@@ -55,7 +57,7 @@ int verify_common(tv::Algo algo, int32_t batch, int32_t num_nodes, int32_t vocab
                    counters};
   int st = tv::validate(a, workspace, workspace_bytes);
   if (st != TV_OK || batch == 0) return st;
-  return tv::launch(a, algo, stream);
+  return tv::launch(a, algo, workspace, stream);
 }
 
 }  // namespace
@@ -63,10 +65,10 @@ int verify_common(tv::Algo algo, int32_t batch, int32_t num_nodes, int32_t vocab
 extern "C" {
 
 size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab) {
-  (void)batch;
-  (void)num_nodes;
-  (void)vocab;
-  return 0;
+  if (batch < 1 || batch > TV_MAX_BATCH || num_nodes < 1 || num_nodes > TV_MAX_NODES ||
+      vocab < 2 || vocab > TV_MAX_VOCAB)
+    return 0;
+  return tv::workspace_layout(batch, vocab).bytes;
 }
 
 int tv_verify(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
@@ -101,7 +103,7 @@ const char* tv_status_string(int code) {
     case TV_OK: return "ok";
     case TV_ERR_INVALID_ARG: return "invalid argument";
     case TV_ERR_UNSUPPORTED: return "unsupported size, temperature or pointer alignment";
-    case TV_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case TV_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     case TV_ERR_HIP: return "HIP kernel launch failed";
     default: return "unknown status";
   }

@@ -1,109 +1,241 @@
 // Traversal Verification (arXiv 2505.12398, Algorithm 3) and the token-level
 // baseline (Sec. 2.2, Algorithm 2 per node) for gfx950 (MI355X, CDNA4).
 //
-// One 1024-thread workgroup verifies one tree. Thread 0 runs the sequential
-// traversal on scalars held in LDS and issues vocabulary-wide passes that all
-// 16 wavefronts execute over the rows of one node, 16 bytes per lane per load:
+// Work split. A workgroup that has no tree claims the next one from a
+// launch-wide counter and becomes its owner: it holds the tree in LDS and
+// runs the sequential traversal on thread 0. Whenever the traversal needs a
+// vocabulary-wide quantity it publishes a batch of passes, each cut into
+// segments of 2048 16-byte vectors of a node's rows; workgroups without a tree
+// claim segments of any published batch (an owner works on its own), compute
+// the segment's partial result and report it. When all segments of its batch
+// are in, the owner combines the partials in segment order and continues. So a
+// tree whose traversal needs many passes is served by many CUs, and the
+// per-tree load imbalance of the method does not leave CUs idle.
 //
-//   STATS   row maxima and sums of 2^(z*k - m*k) (k = log2(e)/T) for the target
-//           and draft rows of a node, plus the parent's logits at each child's
-//           token; run lazily, the first time the traversal descends into a
-//           node whose acceptance rate is above zero;
-//   SPASS   S = sum_x [alpha p(x) - beta q(x)]_+, one per rejection: Eq. (e1)
-//           and (e3) for the rejected node's parent;
-//   SAMPLE  inverse-CDF draw of Y from [A p - B q]_+ (or the target row of an
-//           accepted leaf), in ascending token order.
+// A batch holds the pass the traversal needs now plus the STATS passes of the
+// nodes it will descend into next (the internal nodes on the leftmost
+// remaining path below the next child); those depend only on their own rows,
+// so they run alongside instead of one after another.
+//
+// Pass kinds:
+//   STATS   per row: maximum and sum of 2^(z*k - max*k), k = log2(e)/T, over
+//           the target and draft rows of a node (the target row only for an
+//           accepted leaf); issued the first time the traversal descends into
+//           a node whose acceptance rate is above zero;
+//   SPASS   S = sum_x [alpha p(x) - beta q(x)]_+ over the parent's rows, one per
+//           rejection: Eq. (e1) and (e3);
+//   WSUM    the same weights as SPASS without updating anything (only needed
+//           when Y is drawn at a node whose last pass was not its SPASS).
+// Y is drawn by inverse CDF in ascending token order: the segment partials of
+// the pass that produced the weights locate the segment holding u*W, and the
+// owner rescans that one segment.
 //
 // A node's residual target and draft are never materialised: after k
 // rejections they are b = [A p - B q]_+ and s = c q off the rejected tokens,
-// so four scalars (pi, A, B, rejected draft mass) carry Eq. (e1)-(e3) and a
-// sibling's ratio b/s = [A r - B]_+ / c needs no vocabulary pass. The literal
-// vector form of Algorithm 3 and this four-scalar form give the same values
-// (the CPU tests check it); the traversal order, tests and outputs are those of
-// Algorithm 3.
+// so four scalars (pi, A, B, remaining draft mass) carry Eq. (e1)-(e3) and a
+// sibling's ratio b/s = [A r - B]_+ / c needs no vocabulary pass.
 //
 // Precision. Logits are widened exactly to fp32 and every per-node scalar is
-// fp64. Two element paths: FAST (bf16 logits with V >= 16384) takes each term
-// as the hardware exp2 of an fp32 fma and combines and accumulates in fp64;
-// over a large vocabulary the per-element rounding averages out. PRECISE (fp32
-// logits, or any V < 16384) evaluates every term with fp64 exp2. In both, the
-// remaining draft mass 1 - q(rejected tokens) comes from the pass's own sum of
-// draft terms minus the rejected tokens' terms (recomputed bit-identically),
-// never from 1 - sum q, which cancels when the rejected tokens held most of the
-// draft mass.
+// fp64. FAST (bf16 logits with V >= 16384) takes each term as the hardware
+// exp2 of an fp32 fma and accumulates in fp64; PRECISE (fp32 logits, or any
+// V < 16384) evaluates every term in fp64. The remaining draft mass after Eq.
+// (e2) is the pass's own sum of draft terms minus the rejected tokens' terms,
+// never 1 - sum q(rejected), which cancels when those held most of the mass.
+// Every sum is formed in a fixed order (per thread, then across the
+// workgroup, then across segments), so results do not depend on which
+// workgroup processed which segment.
+//
+// Synchronisation. Data shared between workgroups (segment results, pass
+// parameters) is written with agent-scope atomic stores, which write through
+// to the device-coherent level, and the writer waits for those stores to be
+// acknowledged before it signals (atomic increment of the owner's counter, or
+// atomic store of its work word). This orders data before signal the way an
+// agent-scope release fence would, without the fence's write-back of the
+// whole L2. Readers observe the signal with an atomic load, issue an
+// agent-scope acquire fence and read the data with agent-scope atomic loads.
+// Every wait is bounded by a wall-clock limit after which the launch is
+// abandoned (trees not finished then report TV_TREE_ABORTED), so no wave can
+// spin forever.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "tv.h"
 #include "tv_launch.h"
 
 namespace {
 
-constexpr int kThreads = 1024;
-constexpr int kWaves = kThreads / 64;
-constexpr int kMaxNodes = TV_MAX_NODES;
-constexpr int kMaxBlocks = 2048;   // sampling blocks (64 * bmul vectors each)
-constexpr int kUnroll = 4;         // vectors per row in flight per lane
+constexpr int kNT = 256;                       // threads per workgroup
+constexpr int kNW = kNT / 64;
+constexpr int kSegVec = tv::kSegVec;
+constexpr int kVecPerThread = kSegVec / kNT;   // vectors per row per thread and segment
+// vectors per row in flight per lane: the fp64 element path needs more registers
+template <class A> constexpr int kUnrollOf = A::kPrecise ? 2 : 4;
+constexpr int kCapSmall = 128;                 // node capacity of the compact variant
+constexpr int kCapLarge = TV_MAX_NODES;
+static_assert(kSegVec % (kNT * 4) == 0, "segment must be whole rounds");
+static_assert(tv::kMaxSeg <= 64, "segments are combined by one wavefront");
 
-enum : int { kCmdDone = 0, kCmdStats = 1, kCmdSPass = 2, kCmdSample = 3 };
+// Pass kinds (4 bits each in a batch descriptor) and owner-internal commands.
 enum : int {
-  kPhDescend = 0, kPhTest, kPhAfterSPass, kPhFinal, kPhFinalLeafStats, kPhAfterSample,
-  kPhPinit, kPhTlVisit, kPhTlAfterSPass
+  kCmdNone = 0, kCmdStats2 = 1, kCmdStats1 = 2, kCmdSPass = 3, kCmdSPassSd = 4, kCmdWSum = 5,
+  kCmdLocalSample = 6, kCmdDone = 7
 };
-enum : uint8_t { kFlagStats = 1, kFlagConsulted = 2, kFlagLeafStats = 4, kFlagSd = 8 };
+enum : int { kEvItem = 0, kEvOwn = 1, kEvTree = 2, kEvExit = 3 };
+enum : int {
+  kPhDescend = 0, kPhTest, kPhAfterSPass, kPhFinal, kPhFinalLeafStats, kPhFinalWSum,
+  kPhAfterSample, kPhPinit, kPhTlVisit, kPhTlAfterSPass
+};
+enum : uint8_t { kFlagStats = 1, kFlagConsulted = 2, kFlagBad = 4, kFlagSd = 8 };
 
-struct TreeSmem {
-  // tree structure
-  int16_t parent[kMaxNodes];
-  int16_t depth[kMaxNodes];
-  int16_t child_start[kMaxNodes];
-  int16_t child_list[kMaxNodes];
-  int16_t next_child[kMaxNodes];     // children already removed (always a prefix)
-  int32_t child_count[kMaxNodes];
-  int32_t token[kMaxNodes];
-  float u[kMaxNodes];
-  uint8_t state[kMaxNodes];
-  uint8_t flags[kMaxNodes];
-  float theta[kMaxNodes];
-  // per-node verification state
-  double pi[kMaxNodes];              // current acceptance rate p of the chain ending here
-  double A[kMaxNodes];               // residual target b = [A p - B q]_+
-  double B[kMaxNodes];
-  double rem[kMaxNodes];             // draft mass left after removing rejected tokens
-  double pini[kMaxNodes];
-  double sdsum[kMaxNodes];           // sum of the draft row's terms in its frame
-  double invsb[kMaxNodes];           // 1 / (sum of the target row's terms)
-  double invss[kMaxNodes];           // 1 / (sum of the draft row's terms)
-  double cb[kMaxNodes];              // exponent offset of the target row: -max * k
-  double cs[kMaxNodes];              // exponent offset of the draft row
-  // per-node, about the node's own token at its parent (set by the parent's STATS)
-  double r0[kMaxNodes];              // original ratio p(x) / q(x)
-  double et[kMaxNodes];              // draft term of x in the parent's frame
-  // sampling
-  double blocks[kMaxBlocks];
-  // reductions
-  double red_d[2 * kWaves];
-  float red_f[2 * kWaves];
-  int gather_bad;
-  // command issued by thread 0 for the whole workgroup
-  int cmd, cmd_node, cmd_two_rows, cmd_gather, cmd_sd;
-  double cmd_ap, cmd_bp;             // multipliers of the target / draft terms
-  double cmd_cb, cmd_cs;
-  // pass results
-  float res_m[2];
-  double res_s[2];
-  double res_S;
-  double res_sd;                     // sum of the draft terms of the last SPASS
-  double res_head, res_tail;
-  int res_y;
-  int res_block;
-  int res_bad;
-  // traversal state
-  int phase, cur, accepted, rejected, status, algo;
-  int rows_consulted, resid_passes, tests, pinit_next;
-  double alpha, beta;
+constexpr int kMaxBatch = tv::kMaxBatchPasses;   // passes per batch
+
+// Work word of an owner slot: the batch it offers and how many items are taken.
+// Item i of a batch is segment i % nseg of pass i / nseg.
+//   bits  0-12 items claimed so far (may run past the total: extra claims are void)
+//   bits 13-22 items of the batch (0: nothing offered)
+//   bits 23-29 segments per pass
+//   bits 30-49 tree (batch index)
+//   bits 50-63 sequence number of the batch (low 14 bits), repeated in the descriptor
+struct Work {
+  int cnt, total, nseg, tree, seq;
 };
+__device__ __forceinline__ uint64_t pack_work(int total, int nseg, int tree, int seq) {
+  return (static_cast<uint64_t>(total) << 13) | (static_cast<uint64_t>(nseg) << 23) |
+         (static_cast<uint64_t>(tree) << 30) | (static_cast<uint64_t>(seq & 0x3FFF) << 50);
+}
+__device__ __forceinline__ Work unpack_work(uint64_t w) {
+  return Work{static_cast<int>(w & 0x1FFFu), static_cast<int>((w >> 13) & 0x3FFu),
+              static_cast<int>((w >> 23) & 0x7Fu), static_cast<int>((w >> 30) & 0xFFFFFu),
+              static_cast<int>((w >> 50) & 0x3FFFu)};
+}
+
+// Batch descriptor (8 words per owner slot):
+//   [0..3] multipliers and frames (ap, bp, cb, cs) of the batch's SPASS / WSUM pass
+//   [4], [5] nodes of passes 0-3 and 4-7 (16 bits each)
+//   [6] pass kinds (4 bits each)
+//   [7] sequence number of the batch
+constexpr int kDescWords = 8;
+__device__ __forceinline__ int desc_node(const uint64_t (&d)[kDescWords], int p) {
+  return static_cast<int>((d[4 + (p >> 2)] >> (16 * (p & 3))) & 0xFFFFu);
+}
+__device__ __forceinline__ int desc_cmd(const uint64_t (&d)[kDescWords], int p) {
+  return static_cast<int>((d[6] >> (4 * p)) & 0xFu);
+}
+
+struct Params {
+  const int32_t* parents;
+  const int32_t* tokens;
+  const void* target;
+  const void* draft;
+  const float* uniforms;
+  int32_t* accept_len;
+  int32_t* accepted_node;
+  int32_t* bonus_token;
+  int32_t* status;
+  int8_t* node_state;
+  float* node_theta;
+  float* p_init;
+  int32_t* counters;
+  uint8_t* ws;
+  size_t off_words, off_done, off_desc, off_parts;
+  long long spin_limit;      // wall-clock ticks without progress before the launch is abandoned
+  int batch;
+  int num_nodes;
+  int vocab;
+  int mode;
+  int algo;
+  int grid;                  // workgroups, one workspace slot each
+  int seg_stride;            // partial-result slots per workgroup
+  float k32;                 // log2(e) / T rounded to fp32 (fast element path)
+  double k64;                // log2(e) / T (precise element path)
+};
+
+// A reference into LDS with its address space in the type, so that functions
+// the compiler does not inline still access it with LDS instructions rather
+// than through generic pointers.
+template <class X> using Lds = __attribute__((address_space(3))) X;
+template <class X>
+__device__ __forceinline__ Lds<X>& lds_ref(X& x) {
+  return *reinterpret_cast<Lds<X>*>((__attribute__((address_space(3))) void*)&x);
+}
+
+struct SegPart {             // 32 bytes
+  double s0, s1;
+  float m0, m1;
+  uint32_t pad[2];
+};
+
+// ---------------------------------------------------------------------------
+// Workspace access and synchronisation primitives
+// ---------------------------------------------------------------------------
+
+template <class PP>
+__device__ __forceinline__ uint32_t* ws_remaining(const PP& P) {
+  return reinterpret_cast<uint32_t*>(P.ws);
+}
+template <class PP>
+__device__ __forceinline__ uint32_t* ws_abort(const PP& P) {
+  return reinterpret_cast<uint32_t*>(P.ws + 256);
+}
+template <class PP>
+__device__ __forceinline__ uint32_t* ws_next_tree(const PP& P) {
+  return reinterpret_cast<uint32_t*>(P.ws + 512);
+}
+template <class PP>
+__device__ __forceinline__ uint64_t* ws_words(const PP& P) {
+  return reinterpret_cast<uint64_t*>(P.ws + P.off_words);
+}
+template <class PP>
+__device__ __forceinline__ uint32_t* ws_done(const PP& P) {
+  return reinterpret_cast<uint32_t*>(P.ws + P.off_done);
+}
+template <class PP>
+__device__ __forceinline__ uint64_t* ws_desc(const PP& P, int o) {
+  return reinterpret_cast<uint64_t*>(P.ws + P.off_desc) + kDescWords * static_cast<size_t>(o);
+}
+template <class PP>
+__device__ __forceinline__ SegPart* ws_parts(const PP& P, int o, int pass) {
+  return reinterpret_cast<SegPart*>(P.ws + P.off_parts) +
+         (static_cast<size_t>(o) * kMaxBatch + pass) * P.seg_stride;
+}
+
+__device__ __forceinline__ uint64_t ld_rlx(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_rlx(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_rlx(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_rlx(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_rlx_f64(const double* p) {
+  return __longlong_as_double(static_cast<long long>(
+      ld_rlx(reinterpret_cast<const uint64_t*>(p))));
+}
+__device__ __forceinline__ void st_rlx_f64(double* p, double v) {
+  st_rlx(reinterpret_cast<uint64_t*>(p), static_cast<uint64_t>(__double_as_longlong(v)));
+}
+__device__ __forceinline__ void fence_acquire() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+// Waits until this thread's earlier stores are acknowledged (s_waitcnt
+// vmcnt(0)); with the stores made through st_rlx this orders them before a
+// later signalling atomic. The signal fence keeps the compiler from moving
+// memory operations across it.
+__device__ __forceinline__ void stores_done() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  const uint32_t lo = __shfl(static_cast<uint32_t>(v), src, 64);
+  const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, 64);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
 
 // ---------------------------------------------------------------------------
 // Element access
@@ -141,7 +273,7 @@ struct Geom {
 };
 
 template <typename T>
-__device__ inline Geom row_geom(const T* row, int V) {
+__device__ __forceinline__ Geom row_geom(const T* row, int V) {
   constexpr int E = Elem<T>::E;
   const int mis = static_cast<int>(reinterpret_cast<uintptr_t>(row) & 15);
   int head = mis ? (16 - mis) / static_cast<int>(sizeof(T)) : 0;
@@ -150,68 +282,115 @@ __device__ inline Geom row_geom(const T* row, int V) {
   return Geom{head, rest / E, rest % E};
 }
 
+__device__ __forceinline__ int num_segments(const Geom& g) {
+  const int s = (g.nvec + kSegVec - 1) / kSegVec;
+  return s < 1 ? 1 : s;
+}
+
 template <typename T>
-__device__ inline uint4 load16(const T* row, int head, int v) {
+__device__ __forceinline__ uint4 load16(const T* row, int head, int v) {
   return *reinterpret_cast<const uint4*>(row + head + v * Elem<T>::E);
 }
 
-__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Keeps a loaded vector where it is: without this the compiler may sink a load
+// into the guarded arithmetic that uses it and serialise a round's loads.
+__device__ __forceinline__ void pin(uint4& v) {
+  asm volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+}
 
 // ---------------------------------------------------------------------------
-// Workgroup reductions (fixed order: deterministic)
+// Workgroup reductions (fixed order: deterministic). Results valid in every thread.
 // ---------------------------------------------------------------------------
 
-__device__ inline double wave_sum(double v) {
+struct WgScratch {
+  double red_d[2 * kNW];
+  float red_f[2 * kNW];
+  double scan_d[kNW];
+  int event;
+  int item_owner;
+  uint64_t item_word;
+  uint64_t item_desc[kDescWords];
+  int scan_pos;
+  int new_tree;             // tree just claimed (kEvTree)
+  int trees_left;           // 0 once the tree counter ran past the batch
+  int hit;                  // first thread whose range holds the sample
+  int last_pos;             // last thread with positive weight
+  int smp_seg;
+  double smp_target;        // mass still to cover inside the chosen segment
+};
+
+__device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
   return v;
 }
 
-__device__ inline float wave_max(float v) {
+__device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
   return v;
 }
 
-// Sums of two doubles per thread in one LDS round; results valid in every thread.
-__device__ __forceinline__ void block_sum2(TreeSmem& sm, double& a, double& b) {
+template <class WS>
+__device__ __forceinline__ void block_sum2(WS& ws, double& a, double& b) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   a = wave_sum(a);
   b = wave_sum(b);
   if (lane == 0) {
-    sm.red_d[wave] = a;
-    sm.red_d[kWaves + wave] = b;
+    ws.red_d[wave] = a;
+    ws.red_d[kNW + wave] = b;
   }
   __syncthreads();
   double ta = 0.0, tb = 0.0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    ta += sm.red_d[w];
-    tb += sm.red_d[kWaves + w];
+  for (int w = 0; w < kNW; ++w) {
+    ta += ws.red_d[w];
+    tb += ws.red_d[kNW + w];
   }
   __syncthreads();
   a = ta;
   b = tb;
 }
 
-__device__ __forceinline__ void block_max2(TreeSmem& sm, float& a, float& b) {
+template <class WS>
+__device__ __forceinline__ void block_max2(WS& ws, float& a, float& b) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   a = wave_max(a);
   b = wave_max(b);
   if (lane == 0) {
-    sm.red_f[wave] = a;
-    sm.red_f[kWaves + wave] = b;
+    ws.red_f[wave] = a;
+    ws.red_f[kNW + wave] = b;
   }
   __syncthreads();
   float ta = -INFINITY, tb = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    ta = fmaxf(ta, sm.red_f[w]);
-    tb = fmaxf(tb, sm.red_f[kWaves + w]);
+  for (int w = 0; w < kNW; ++w) {
+    ta = fmaxf(ta, ws.red_f[w]);
+    tb = fmaxf(tb, ws.red_f[kNW + w]);
   }
   __syncthreads();
   a = ta;
   b = tb;
+}
+
+// Inclusive scan over the threads of the workgroup in thread order.
+template <class WS>
+__device__ __forceinline__ double block_incl_scan(WS& ws, double v) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) ws.scan_d[wave] = incl;
+  __syncthreads();
+  double base = 0.0;
+  for (int w = 0; w < wave; ++w) base += ws.scan_d[w];
+  __syncthreads();
+  return base + incl;
 }
 
 // ---------------------------------------------------------------------------
@@ -239,14 +418,10 @@ struct PreciseArith {              // fp64 throughout
   __device__ double kd() const { return k; }
 };
 
-// ---------------------------------------------------------------------------
-// STATS: row maximum and sum of terms, online over one read of the row
-// ---------------------------------------------------------------------------
-
-// Running state of one thread over a row. Before the first finite value the
-// maximum is -inf and the frame is that of a finite sentinel, so -inf entries
-// add 2^-inf = 0 with no branch, a NaN or +inf entry turns the sum into NaN,
-// and a row with no finite entry keeps maximum -inf.
+// Running maximum and sum of one thread over a row. Before the first finite
+// value the maximum is -inf and the frame is that of a finite sentinel, so
+// -inf entries add 2^-inf = 0 with no branch, a NaN or +inf entry turns the
+// sum into NaN, and a row with no finite entry keeps maximum -inf.
 constexpr float kFrameSentinel = -1.0e30f;
 
 struct Online {
@@ -260,8 +435,6 @@ __device__ __forceinline__ Online online_init(const A& ar) {
   return Online{-INFINITY, ar.frame(kFrameSentinel), 0.0};
 }
 
-// Raise the running maximum to at least vmax (rescaling the sum), then add the
-// terms of x[0..n).
 template <class A>
 __device__ __forceinline__ void online_raise(Online& o, float vmax, const A& ar) {
   if (vmax > o.m) {
@@ -277,7 +450,11 @@ __device__ __forceinline__ void online_raise(Online& o, float vmax, const A& ar)
 }
 
 template <class A, int N>
-__device__ __forceinline__ void online_sum(Online& o, const float (&x)[N], const A& ar) {
+__device__ __forceinline__ void online_add(Online& o, const float (&x)[N], const A& ar) {
+  float vmax = x[0];
+#pragma unroll
+  for (int e = 1; e < N; ++e) vmax = fmaxf(vmax, x[e]);
+  online_raise(o, vmax, ar);
   if constexpr (A::kPrecise) {
 #pragma unroll
     for (int e = 0; e < N; ++e) o.s += ar.ex(x[e], o.c);
@@ -290,120 +467,9 @@ __device__ __forceinline__ void online_sum(Online& o, const float (&x)[N], const
   }
 }
 
-template <int N>
-__device__ __forceinline__ float vec_max(const float (&x)[N]) {
-  float m = x[0];
-#pragma unroll
-  for (int e = 1; e < N; ++e) m = fmaxf(m, x[e]);
-  return m;
-}
-
-template <typename T, class A, bool TWO>
-__device__ __forceinline__ void stats_pass(TreeSmem& sm, const T* rb, const T* rs, int V,
-                                           const A& ar, int node, bool gather) {
-  constexpr int E = Elem<T>::E;
-  const int tid = threadIdx.x;
-  // The parent's logits at its children's tokens: loaded now, used after the
-  // reduction (by the same threads), so the row stream does not wait on them.
-  const bool gthread = gather && tid < sm.child_count[node];
-  int gchild = 0;
-  float gb = 0.0f, gs = 0.0f;
-  if (gthread) {
-    gchild = sm.child_list[sm.child_start[node] + tid];
-    const int x = sm.token[gchild];
-    gb = Elem<T>::scalar(rb + x);
-    gs = Elem<T>::scalar(rs + x);
-  }
-  const Geom g = row_geom(rb, V);
-  Online ob = online_init(ar), os = online_init(ar);
-  auto scalar_elem = [&](int i) {
-    float xb[1] = {Elem<T>::scalar(rb + i)};
-    online_raise(ob, xb[0], ar);
-    online_sum(ob, xb, ar);
-    if constexpr (TWO) {
-      float xs[1] = {Elem<T>::scalar(rs + i)};
-      online_raise(os, xs[0], ar);
-      online_sum(os, xs, ar);
-    }
-  };
-  if (tid < g.head) scalar_elem(tid);
-  if (tid < g.tail) scalar_elem(g.head + g.nvec * E + tid);
-  for (int v0 = tid; v0 < g.nvec; v0 += kThreads * kUnroll) {
-    uint4 lb[kUnroll], ls[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int v = v0 + u * kThreads;
-      if (v < g.nvec) {
-        lb[u] = load16(rb, g.head, v);
-        if constexpr (TWO) ls[u] = load16(rs, g.head, v);
-      }
-    }
-    // one rescale per group of kUnroll vectors and row
-    float xb[kUnroll][E], xs[kUnroll][E];
-    float mb = -INFINITY, ms = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      if (v0 + u * kThreads < g.nvec) {
-        Elem<T>::unpack(lb[u], xb[u]);
-        mb = fmaxf(mb, vec_max(xb[u]));
-        if constexpr (TWO) {
-          Elem<T>::unpack(ls[u], xs[u]);
-          ms = fmaxf(ms, vec_max(xs[u]));
-        }
-      }
-    }
-    online_raise(ob, mb, ar);
-    if constexpr (TWO) online_raise(os, ms, ar);
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      if (v0 + u * kThreads < g.nvec) {
-        online_sum(ob, xb[u], ar);
-        if constexpr (TWO) online_sum(os, xs[u], ar);
-      }
-    }
-  }
-  // both rows' maxima in one round, then both rows' sums in one round
-  float Mb = ob.m, Ms = TWO ? os.m : -INFINITY;
-  block_max2(sm, Mb, Ms);
-  const double Cb = ar.frame(Mb);
-  const double Cs = TWO ? ar.frame(Ms) : 0.0;
-  // exact fp64 change of frame; a thread that saw no finite value has s = 0
-  // (or NaN) and a factor 0 unless the whole row has no finite value
-  double Sb = ob.s * exp2(Cb - ob.c);
-  double Ss = TWO ? os.s * exp2(Cs - os.c) : 0.0;
-  block_sum2(sm, Sb, Ss);
-  const bool bad = !(Mb > -INFINITY) || !isfinite(Sb) ||
-                   (TWO && (!(Ms > -INFINITY) || !isfinite(Ss)));
-  if (tid == 0) {
-    sm.cb[node] = Cb;
-    sm.invsb[node] = 1.0 / Sb;
-    if constexpr (TWO) {
-      sm.cs[node] = Cs;
-      sm.invss[node] = 1.0 / Ss;
-    }
-    sm.res_bad = bad ? 1 : 0;
-    sm.gather_bad = 0;
-  }
-  __syncthreads();
-  // Children's original ratios r0 = p(x)/q(x) and draft terms, one thread each.
-  if (gthread && !bad) {
-    const double kd = ar.kd();
-    const double lp = fma(static_cast<double>(gb), kd, Cb) - log2(Sb);
-    const double lq = fma(static_cast<double>(gs), kd, Cs) - log2(Ss);
-    sm.r0[gchild] = exp2(lp - lq);
-    sm.et[gchild] = ar.ex(gs, Cs);
-    if (gs == -INFINITY) sm.gather_bad = 1;     // token the draft cannot produce
-  }
-  __syncthreads();
-  if (tid == 0 && sm.gather_bad) sm.res_bad = 1;
-}
-
-// ---------------------------------------------------------------------------
 // Residual weights max(ap * tb - bp * ts, 0), tb and ts the target and draft
 // terms of an element (TWO == false: target only, weight ap * tb). With SD the
 // draft terms are also summed, exactly in fp64.
-// ---------------------------------------------------------------------------
-
 struct TermParams {
   double cb, cs;   // frames of the target and draft rows
   double ap, bp;   // multipliers of the target and draft terms
@@ -411,9 +477,8 @@ struct TermParams {
 
 template <class A, bool TWO, bool SD> struct Terms;
 
-// Fast path: fp32 per element; the weights of one vector are summed in fp32
-// and the vector sums in fp64.
 template <bool TWO, bool SD> struct Terms<FastArith, TWO, SD> {
+  using W = float;
   float k, cb, cs, ap, bp;
   __device__ Terms(const FastArith& ar, const TermParams& p)
       : k(ar.k), cb(static_cast<float>(p.cb)), cs(static_cast<float>(p.cs)),
@@ -445,8 +510,8 @@ template <bool TWO, bool SD> struct Terms<FastArith, TWO, SD> {
   }
 };
 
-// Precise path: fp64 throughout.
 template <bool TWO, bool SD> struct Terms<PreciseArith, TWO, SD> {
+  using W = double;
   double k, cb, cs, ap, bp;
   __device__ Terms(const PreciseArith& ar, const TermParams& p)
       : k(ar.k), cb(p.cb), cs(p.cs), ap(p.ap), bp(p.bp) {}
@@ -477,14 +542,16 @@ template <bool TWO, bool SD> struct Terms<PreciseArith, TWO, SD> {
   }
 };
 
+// One unit of a segment: a scalar element or a 16-byte vector.
 template <typename T, class TM, bool TWO>
 __device__ __forceinline__ double vec_sum(const TM& tm, const uint4& vb, const uint4& vs,
                                           double& sd) {
   constexpr int E = Elem<T>::E;
   float xb[E], xs[E];
   Elem<T>::unpack(vb, xb);
-  if constexpr (TWO) Elem<T>::unpack(vs, xs);
-  else {
+  if constexpr (TWO) {
+    Elem<T>::unpack(vs, xs);
+  } else {
 #pragma unroll
     for (int e = 0; e < E; ++e) xs[e] = 0.0f;
   }
@@ -499,227 +566,199 @@ __device__ __forceinline__ double scalar_weight(const TM& tm, const T* rb, const
   return tm.sum(xb, xs, sd);
 }
 
-// S = sum of the residual weights (Eq. e1, e3); with SD also the draft-term sum.
-template <typename T, class A, bool SD>
-__device__ __forceinline__ void s_pass(TreeSmem& sm, const T* rb, const T* rs, int V,
-                                       const A& ar, const TermParams& p) {
-  const Terms<A, true, SD> tm(ar, p);
+// ---------------------------------------------------------------------------
+// Segment passes (any workgroup). Thread t takes vectors vb + t + i * kNT of
+// the segment; segment 0 also holds the head elements and the last segment
+// the tail elements. Per thread: head, vectors in order, tail.
+// ---------------------------------------------------------------------------
+
+struct SegRange {
+  int vb, ve;          // vectors [vb, ve)
+  bool first, last;
+};
+
+__device__ __forceinline__ SegRange seg_range(const Geom& g, int seg, int nseg) {
+  SegRange r;
+  r.vb = seg * kSegVec;
+  r.ve = min(g.nvec, r.vb + kSegVec);
+  r.first = seg == 0;
+  r.last = seg == nseg - 1;
+  return r;
+}
+
+template <typename T, class A, bool TWO>
+__device__ void seg_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
+                          const SegRange& r, const A& ar, SegPart& out) {
+  constexpr int E = Elem<T>::E;
+  constexpr int kUnroll = kUnrollOf<A>;
   const int tid = threadIdx.x;
-  const Geom g = row_geom(rb, V);
-  double acc = 0.0, sd = 0.0;
-  if (tid < g.head) acc += scalar_weight<T, decltype(tm), true>(tm, rb, rs, tid, sd);
-  const int tail0 = g.head + g.nvec * Elem<T>::E;
-  if (tid < g.tail) acc += scalar_weight<T, decltype(tm), true>(tm, rb, rs, tail0 + tid, sd);
-  for (int v0 = tid; v0 < g.nvec; v0 += kThreads * kUnroll) {
+  Online ob = online_init(ar), os = online_init(ar);
+  if (r.first && tid < g.head) {
+    float xb[1] = {Elem<T>::scalar(rb + tid)};
+    online_add(ob, xb, ar);
+    if constexpr (TWO) {
+      float xs[1] = {Elem<T>::scalar(rs + tid)};
+      online_add(os, xs, ar);
+    }
+  }
+  // Loads are unconditional (indices clamped into the segment) so that all of
+  // a round's loads are in flight together; only the arithmetic is guarded.
+#pragma unroll 1
+  for (int i0 = 0; i0 < kVecPerThread && i0 * kNT < r.ve - r.vb; i0 += kUnroll) {
     uint4 lb[kUnroll], ls[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int v = v0 + u * kThreads;
-      if (v < g.nvec) {
-        lb[u] = load16(rb, g.head, v);
-        ls[u] = load16(rs, g.head, v);
-      }
+      const int v = min(r.vb + tid + (i0 + u) * kNT, r.ve - 1);
+      lb[u] = load16(rb, g.head, v);
+      if constexpr (TWO) ls[u] = load16(rs, g.head, v);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int v = v0 + u * kThreads;
-      if (v < g.nvec) acc += vec_sum<T, decltype(tm), true>(tm, lb[u], ls[u], sd);
+      pin(lb[u]);
+      if constexpr (TWO) pin(ls[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int v = r.vb + tid + (i0 + u) * kNT;
+      if (v < r.ve) {
+        float x[E];
+        Elem<T>::unpack(lb[u], x);
+        online_add(ob, x, ar);
+        if constexpr (TWO) {
+          Elem<T>::unpack(ls[u], x);
+          online_add(os, x, ar);
+        }
+      }
     }
   }
-  block_sum2(sm, acc, sd);
-  if (tid == 0) {
-    sm.res_S = acc;
-    if constexpr (SD) sm.res_sd = sd;
+  if (r.last && tid < g.tail) {
+    const int i = g.head + g.nvec * E + tid;
+    float xb[1] = {Elem<T>::scalar(rb + i)};
+    online_add(ob, xb, ar);
+    if constexpr (TWO) {
+      float xs[1] = {Elem<T>::scalar(rs + i)};
+      online_add(os, xs, ar);
+    }
   }
-  __syncthreads();
+  float Mb = ob.m, Ms = TWO ? os.m : -INFINITY;
+  block_max2(ws, Mb, Ms);
+  // exact fp64 change of frame; a thread that saw no finite value has s = 0
+  // (or NaN) and the factor 0. A segment with no finite value keeps s = 0 (or
+  // NaN) and maximum -inf.
+  double Sb = (Mb > -INFINITY) ? ob.s * exp2(ar.frame(Mb) - ob.c) : ob.s;
+  double Ss = (TWO && Ms > -INFINITY) ? os.s * exp2(ar.frame(Ms) - os.c) : (TWO ? os.s : 0.0);
+  block_sum2(ws, Sb, Ss);
+  out.m0 = Mb;
+  out.m1 = Ms;
+  out.s0 = Sb;
+  out.s1 = Ss;
+}
+
+template <typename T, class A, bool SD>
+__device__ void seg_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
+                         const SegRange& r, const A& ar, const TermParams& p, SegPart& out) {
+  const Terms<A, true, SD> tm(ar, p);
+  using TM = Terms<A, true, SD>;
+  constexpr int kUnroll = kUnrollOf<A>;
+  const int tid = threadIdx.x;
+  double acc = 0.0, sd = 0.0;
+  if (r.first && tid < g.head) acc += scalar_weight<T, TM, true>(tm, rb, rs, tid, sd);
+#pragma unroll 1
+  for (int i0 = 0; i0 < kVecPerThread && i0 * kNT < r.ve - r.vb; i0 += kUnroll) {
+    uint4 lb[kUnroll], ls[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int v = min(r.vb + tid + (i0 + u) * kNT, r.ve - 1);
+      lb[u] = load16(rb, g.head, v);
+      ls[u] = load16(rs, g.head, v);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      pin(lb[u]);
+      pin(ls[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int v = r.vb + tid + (i0 + u) * kNT;
+      if (v < r.ve) acc += vec_sum<T, TM, true>(tm, lb[u], ls[u], sd);
+    }
+  }
+  if (r.last && tid < g.tail)
+    acc += scalar_weight<T, TM, true>(tm, rb, rs, g.head + g.nvec * Elem<T>::E + tid, sd);
+  block_sum2(ws, acc, sd);
+  out.s0 = acc;
+  out.s1 = sd;
+  out.m0 = 0.0f;
+  out.m1 = 0.0f;
 }
 
 // ---------------------------------------------------------------------------
-// SAMPLE: inverse CDF over the residual weights, ascending token order.
-// Order of the running sum: head elements, then blocks of 64 vectors (one per
-// wavefront and iteration), then tail elements.
+// Owner state (LDS) and the scalar traversal logic (thread 0)
 // ---------------------------------------------------------------------------
 
-template <typename T, class A, bool TWO>
-__device__ __forceinline__ void sample_pass(TreeSmem& sm, const T* rb, const T* rs, int V,
-                                            const A& ar, const TermParams& p, float u) {
-  constexpr int E = Elem<T>::E;
-  constexpr int kU = 2;            // iterations (vectors per lane) in flight
-  const Terms<A, TWO, false> tm(ar, p);
-  using TM = Terms<A, TWO, false>;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const Geom g = row_geom(rb, V);
-  const int tail0 = g.head + g.nvec * E;
-  const int nblocks = (g.nvec + 63) / 64;
-  const int iters = (g.nvec + kThreads - 1) / kThreads;
-  double unused = 0.0;
-  for (int it0 = 0; it0 < iters; it0 += kU) {
-    uint4 lb[kU], ls[kU];
-#pragma unroll
-    for (int q = 0; q < kU; ++q) {
-      const int v = (it0 + q) * kThreads + tid;
-      lb[q] = make_uint4(0, 0, 0, 0);
-      ls[q] = make_uint4(0, 0, 0, 0);
-      if (v < g.nvec) {
-        lb[q] = load16(rb, g.head, v);
-        if constexpr (TWO) ls[q] = load16(rs, g.head, v);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < kU; ++q) {
-      if (it0 + q < iters) {
-        const int v = (it0 + q) * kThreads + tid;
-        double l = v < g.nvec ? vec_sum<T, TM, TWO>(tm, lb[q], ls[q], unused) : 0.0;
-        l = wave_sum(l);
-        const int blk = (it0 + q) * kWaves + wave;
-        if (lane == 0 && blk < nblocks) sm.blocks[blk] = l;
-      }
-    }
-  }
-  if (tid == 0) {
-    double h = 0.0, tl = 0.0;
-    for (int i = 0; i < g.head; ++i) h += scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
-    for (int i = tail0; i < V; ++i) tl += scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
-    sm.res_head = h;
-    sm.res_tail = tl;
-  }
-  __syncthreads();
-  // Thread 0 locates the segment holding u * W (W accumulated in scan order).
-  if (tid == 0) {
-    double W = sm.res_head;
-    for (int b = 0; b < nblocks; ++b) W += sm.blocks[b];
-    W += sm.res_tail;
-    const double target = static_cast<double>(u) * W;
-    int y = -1;
-    int found_block = -1;
-    double base = 0.0;
-    if (!(W > 0.0)) {
-      y = -2;                                        // no mass: degenerate
-    } else {
-      double C = 0.0;
-      for (int i = 0; i < g.head && y < 0; ++i) {
-        const double w = scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
-        if (target < C + w) y = i;
-        C += w;
-      }
-      if (y < 0) {
-        for (int b = 0; b < nblocks; ++b) {
-          if (target < C + sm.blocks[b]) {
-            found_block = b;
-            base = C;
-            break;
-          }
-          C += sm.blocks[b];
-        }
-      }
-      if (y < 0 && found_block < 0) {
-        int last = -1;
-        for (int i = tail0; i < V; ++i) {
-          const double w = scalar_weight<T, TM, TWO>(tm, rb, rs, i, unused);
-          if (w > 0.0) last = i;
-          if (target < C + w) { y = i; break; }
-          C += w;
-        }
-        if (y < 0) y = last;   // rounding at the very end: last positive weight
-      }
-    }
-    sm.res_y = y;
-    sm.res_block = found_block;
-    sm.res_S = target - base;   // mass still to cover inside the block
-  }
-  __syncthreads();
-  const int blk = sm.res_block;
-  if (blk >= 0 && wave == 0) {
-    const int v = blk * 64 + lane;
-    double l = 0.0;
-    double wd[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) wd[e] = 0.0;
-    if (v < g.nvec) {
-      const uint4 vb = load16(rb, g.head, v);
-      uint4 vs = make_uint4(0, 0, 0, 0);
-      if constexpr (TWO) vs = load16(rs, g.head, v);
-      float xb[E], xs[E];
-      Elem<T>::unpack(vb, xb);
-      Elem<T>::unpack(vs, xs);
-      // the same per-element weights (and vector sum) as in the pass above
-      if constexpr (A::kPrecise) {
-        double w[E];
-        tm.weights(xb, xs, w, unused);
-#pragma unroll
-        for (int e = 0; e < E; ++e) wd[e] = w[e];
-      } else {
-        float w[E];
-        tm.weights(xb, xs, w, unused);
-#pragma unroll
-        for (int e = 0; e < E; ++e) wd[e] = static_cast<double>(w[e]);
-      }
-      l = vec_sum<T, TM, TWO>(tm, vb, vs, unused);
-    }
-    // inclusive scan over lanes
-    double incl = l;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const double o = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += o;
-    }
-    const double excl = incl - l;
-    const double rem = sm.res_S;
-    const bool hit = rem < incl && l > 0.0;
-    const unsigned long long hits = __ballot(hit);
-    int chosen_lane;
-    if (hits) {
-      chosen_lane = __ffsll(static_cast<long long>(hits)) - 1;
-    } else {
-      const unsigned long long pos = __ballot(l > 0.0);
-      chosen_lane = pos ? 63 - __clzll(static_cast<long long>(pos)) : -1;
-    }
-    if (lane == chosen_lane) {
-      double C = excl;
-      int y = -1, last = -1;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        if (y < 0) {
-          if (wd[e] > 0.0) last = e;
-          if (rem < C + wd[e] && wd[e] > 0.0) y = e;
-          C += wd[e];
-        }
-      }
-      if (y < 0) y = last;
-      sm.res_y = g.head + v * E + y;
-    }
-  }
-  __syncthreads();
-}
+enum : int { kCmdBatch = 8 };      // controller command: publish the batch in sm.b*
 
-// ---------------------------------------------------------------------------
-// Scalar traversal logic (thread 0)
-// ---------------------------------------------------------------------------
-
-struct Params {
-  const int32_t* parents;
-  const int32_t* tokens;
-  const void* target;
-  const void* draft;
-  const float* uniforms;
-  int32_t* accept_len;
-  int32_t* accepted_node;
-  int32_t* bonus_token;
-  int32_t* status;
-  int8_t* node_state;
-  float* node_theta;
-  float* p_init;
-  int32_t* counters;
-  int num_nodes;
-  int vocab;
-  int mode;
-  float k32;      // log2(e) / T rounded to fp32 (fast element path)
-  double k64;     // log2(e) / T (precise element path)
+template <int kCap>
+struct TreeSmem {
+  // tree structure
+  int16_t parent[kCap];
+  int16_t depth[kCap];
+  int16_t child_start[kCap];
+  int16_t child_list[kCap];
+  int16_t next_child[kCap];        // children already removed (always a prefix)
+  int32_t child_count[kCap];
+  int32_t token[kCap];
+  float u[kCap];
+  float theta[kCap];
+  float gb[kCap], gs[kCap];        // parent's target / draft logit at the node's token
+                                   // (gathered when the tree is loaded)
+  uint8_t state[kCap];
+  uint8_t flags[kCap];
+  // per-node verification state
+  double pi[kCap];                 // current acceptance rate p of the chain ending here
+  double A[kCap];                  // residual target b = [A p - B q]_+
+  double B[kCap];
+  double rem[kCap];                // draft mass left after removing rejected tokens
+  double pini[kCap];
+  double sdsum[kCap];              // sum of the draft row's terms in its frame
+  double invsb[kCap];              // 1 / (sum of the target row's terms)
+  double invss[kCap];              // 1 / (sum of the draft row's terms)
+  double cb[kCap];                 // exponent offset of the target row: -max * k
+  double cs[kCap];                 // exponent offset of the draft row
+  double r0[kCap];                 // original ratio p(x) / q(x) of the node's token at its parent
+  double et[kCap];                 // draft term of the node's token in the parent's frame
+  // traversal state (held in registers while the controller runs)
+  int has_tree, tree;
+  int phase, cur, accepted, rejected, status;
+  int rows_consulted, resid_passes, tests, pinit_next;
+  double alpha, beta;
+  // command from the controller; a batch: pass 0 is the one the traversal
+  // waits for, the others are STATS of nodes it will descend into
+  int cmd;
+  int bn;
+  int16_t bnode[kMaxBatch];
+  int8_t bcmd[kMaxBatch];
+  double cmd_ap, cmd_bp, cmd_cb, cmd_cs;    // parameters of a SPASS / WSUM pass 0
+  // the batch in flight, then just completed
+  int pending, bnseg;
+  uint32_t seq;                    // batches published by this workgroup
+  uint32_t expect_done;            // value of this slot's done counter that completes the batch
+  uint64_t desc[kDescWords];       // the published descriptor (the owner claims from it)
+  int spass_node;                  // node whose SPASS partials are in the workspace (-1: none)
+  double last_ap, last_bp, last_cb, last_cs;
+  // local sample request
+  int smp_from_stats;              // segment weights from a STATS pass (accepted leaf)
+  int smp_two;
+  double smp_ap, smp_bp, smp_cb, smp_cs;
+  // results of the combine
+  double res_S, res_sd;
+  int res_y;
 };
 
 // Chain rate of child c given its parent j's current state:
 // min(pi_j * b_j(x)/s_j(x), 1) with b/s = [A r - B]_+ * (remaining draft mass).
-__device__ inline double child_rate(const TreeSmem& sm, int mode, int j, int c) {
+template <int kCap>
+__device__ inline double child_rate(const Lds<TreeSmem<kCap>>& sm, int mode, int j, int c) {
   if (sm.pi[j] == 0.0) return 0.0;
   double v = fmax(sm.A[j] * sm.r0[c] - sm.B[j], 0.0);
   if (mode == TV_SIBLINGS_WITHOUT_REPLACEMENT) v *= sm.rem[j];
@@ -730,8 +769,10 @@ __device__ inline double child_rate(const TreeSmem& sm, int mode, int j, int c) 
 // After a pass at j that rejected a child: draft mass left once every rejected
 // child's token is removed (Eq. e2 applied to all of them), from the pass's own
 // draft-term sum minus those tokens' terms, computed the same way.
-__device__ inline void update_remaining_mass(TreeSmem& sm, int j) {
-  if (sm.cmd_sd) {
+template <int kCap>
+__device__ inline void update_remaining_mass(Lds<TreeSmem<kCap>>& sm, int j,
+                                             bool pass_summed_draft) {
+  if (pass_summed_draft) {
     sm.sdsum[j] = sm.res_sd;
     sm.flags[j] |= kFlagSd;
   }
@@ -742,109 +783,164 @@ __device__ inline void update_remaining_mass(TreeSmem& sm, int j) {
   sm.rem[j] = (total - removed) / total;
 }
 
-__device__ inline void issue_stats(TreeSmem& sm, int node, bool two, bool gather) {
-  sm.cmd = kCmdStats;
-  sm.cmd_node = node;
-  sm.cmd_two_rows = two ? 1 : 0;
-  sm.cmd_gather = gather ? 1 : 0;
+template <int kCap>
+__device__ inline void batch_begin(Lds<TreeSmem<kCap>>& sm, int cmd, int node) {
+  sm.cmd = kCmdBatch;
+  sm.bn = 1;
+  sm.bnode[0] = static_cast<int16_t>(node);
+  sm.bcmd[0] = static_cast<int8_t>(cmd);
+  sm.cmd_ap = sm.cmd_bp = sm.cmd_cb = sm.cmd_cs = 0.0;
 }
 
-__device__ inline void issue_spass(TreeSmem& sm, int node, double alpha, double beta, bool wo) {
-  sm.cmd = kCmdSPass;
-  sm.cmd_node = node;
-  sm.cmd_two_rows = 1;
-  sm.cmd_sd = (wo && !(sm.flags[node] & kFlagSd)) ? 1 : 0;
+// Adds STATS of the internal nodes without statistics on the leftmost
+// remaining path from c: the traversal descends through them next.
+template <int kCap>
+__device__ inline void batch_add_descent(Lds<TreeSmem<kCap>>& sm, int c) {
+  while (sm.bn < kMaxBatch && sm.child_count[c] > 0 && sm.next_child[c] < sm.child_count[c]) {
+    if (!(sm.flags[c] & kFlagStats)) {
+      sm.bnode[sm.bn] = static_cast<int16_t>(c);
+      sm.bcmd[sm.bn] = static_cast<int8_t>(kCmdStats2);
+      ++sm.bn;
+    }
+    c = sm.child_list[sm.child_start[c] + sm.next_child[c]];
+  }
+}
+
+// STATS of node j (two rows, or the target row of an accepted leaf); with
+// `descent`, also of the internal nodes below j the traversal reaches next.
+template <int kCap>
+__device__ inline void issue_stats(Lds<TreeSmem<kCap>>& sm, int node, bool two, bool descent) {
+  batch_begin(sm, two ? kCmdStats2 : kCmdStats1, node);
+  if (descent && sm.next_child[node] < sm.child_count[node])
+    batch_add_descent(sm, sm.child_list[sm.child_start[node] + sm.next_child[node]]);
+}
+
+// SPASS at j (a child of j was just rejected); with `descent`, also STATS of
+// the internal nodes the traversal descends into after it: j's next child c
+// and the leftmost path below it, if c's chain rate stays above zero. That
+// rate is [A' r(c) - B']_+ with A' = alpha / S, B' = beta / S, so its sign is
+// known before S is: it is positive iff alpha r(c) > beta.
+template <int kCap>
+__device__ inline void issue_spass(Lds<TreeSmem<kCap>>& sm, int node, double alpha, double beta,
+                                   bool wo, bool descent) {
+  batch_begin(sm, (wo && !(sm.flags[node] & kFlagSd)) ? kCmdSPassSd : kCmdSPass, node);
   sm.cmd_ap = alpha * sm.invsb[node];
   sm.cmd_bp = beta * sm.invss[node];
   sm.cmd_cb = sm.cb[node];
   sm.cmd_cs = sm.cs[node];
-}
-
-__device__ inline void issue_sample(TreeSmem& sm, int node, bool leaf) {
-  sm.cmd = kCmdSample;
-  sm.cmd_node = node;
-  sm.cmd_cb = sm.cb[node];
-  if (leaf) {
-    sm.cmd_two_rows = 0;
-    sm.cmd_ap = 1.0;
-    sm.cmd_bp = 0.0;
-    sm.cmd_cs = 0.0;
-  } else {
-    sm.cmd_two_rows = 1;
-    sm.cmd_ap = sm.A[node] * sm.invsb[node];
-    sm.cmd_bp = sm.B[node] * sm.invss[node];
-    sm.cmd_cs = sm.cs[node];
+  if (descent && sm.next_child[node] < sm.child_count[node]) {
+    const int c = sm.child_list[sm.child_start[node] + sm.next_child[node]];
+    if (alpha * sm.r0[c] > beta) batch_add_descent(sm, c);
   }
 }
 
-__device__ inline void fail(TreeSmem& sm, int status) {
+template <int kCap>
+__device__ inline void request_sample(Lds<TreeSmem<kCap>>& sm, bool from_stats, bool two,
+                                      double ap, double bp, double cb, double cs) {
+  sm.cmd = kCmdLocalSample;
+  sm.smp_from_stats = from_stats ? 1 : 0;
+  sm.smp_two = two ? 1 : 0;
+  sm.smp_ap = ap;
+  sm.smp_bp = bp;
+  sm.smp_cb = cb;
+  sm.smp_cs = cs;
+}
+
+template <int kCap>
+__device__ inline void fail(Lds<TreeSmem<kCap>>& sm, int status) {
   sm.status = status;
   sm.cmd = kCmdDone;
 }
 
-__device__ inline void init_node_state(TreeSmem& sm, int c, double pi) {
+template <int kCap>
+__device__ inline void init_node_state(Lds<TreeSmem<kCap>>& sm, int c, double pi) {
   sm.pi[c] = pi;
   sm.A[c] = 1.0;
   sm.B[c] = 0.0;
   sm.rem[c] = 1.0;
 }
 
-// Runs until the next vocabulary pass is needed (or the tree is done).
-template <class A>
-__device__ __attribute__((noinline)) void advance(TreeSmem& sm, const Params& P, const A& ar) {
-  if (sm.cmd == kCmdStats) {
-    const int j = sm.cmd_node;
-    if (sm.res_bad) { fail(sm, TV_TREE_NONFINITE); return; }
-    if (sm.cmd_two_rows) sm.flags[j] |= kFlagStats;
-    else sm.flags[j] |= kFlagLeafStats;
-  }
+struct TraversalArgs {
+  int num_nodes, mode, algo;
+};
+
+struct Ctl {
+  int phase, cur, accepted, rejected, rows, resid, tests, pinit_next;
+  double alpha, beta;
+};
+
+// Runs until the next batch of passes or a local sample is needed, or the tree
+// is done. `done_cmd` is the kind of pass 0 of the batch (or the local sample)
+// whose result is in sm.res_*; STATS results are already in the node arrays.
+template <int kCap>
+__device__ __forceinline__ void advance_impl(Lds<TreeSmem<kCap>>& sm, TraversalArgs P,
+                                             int done_cmd, Ctl& ct) {
+  const bool summed_draft = done_cmd == kCmdSPassSd;
   const bool wo = P.mode == TV_SIBLINGS_WITHOUT_REPLACEMENT;
+  const bool tv_algo = P.algo == static_cast<int>(tv::Algo::kTraversal);
   for (;;) {
-    switch (sm.phase) {
+    switch (ct.phase) {
       // ---- Alg. 3 initial chain rates for the p_init output -------------
       case kPhPinit: {
-        while (sm.pinit_next < P.num_nodes && sm.child_count[sm.pinit_next] == 0)
-          ++sm.pinit_next;
-        if (sm.pinit_next < P.num_nodes) {
-          const int j = sm.pinit_next;
-          if (!(sm.flags[j] & kFlagStats)) { issue_stats(sm, j, true, true); return; }
-          ++sm.pinit_next;
-          continue;
+        // STATS of every node with children, up to a batch at a time
+        int first = -1, n = 0;
+        for (int j = ct.pinit_next; j < P.num_nodes; ++j) {
+          if (sm.child_count[j] == 0 || (sm.flags[j] & kFlagStats)) continue;
+          if (n == kMaxBatch) break;
+          if (first < 0) {
+            batch_begin(sm, kCmdStats2, j);
+            first = j;
+          } else {
+            sm.bnode[sm.bn] = static_cast<int16_t>(j);
+            sm.bcmd[sm.bn] = static_cast<int8_t>(kCmdStats2);
+            ++sm.bn;
+          }
+          ++n;
         }
+        if (n > 0) {
+          ct.pinit_next = first;
+          return;
+        }
+        for (int j = 0; j < P.num_nodes; ++j)
+          if (sm.child_count[j] > 0 && (sm.flags[j] & kFlagBad)) {
+            fail(sm, TV_TREE_NONFINITE);
+            return;
+          }
         sm.pini[0] = 1.0;
         for (int i = 1; i < P.num_nodes; ++i) {
           const int j = sm.parent[i];
           if (sm.pini[j] == 0.0) { sm.pini[i] = 0.0; continue; }
           sm.pini[i] = fmin(sm.pini[j] * sm.r0[i], 1.0);
         }
-        sm.phase = sm.algo == static_cast<int>(tv::Algo::kTraversal) ? kPhDescend : kPhTlVisit;
+        ct.phase = tv_algo ? kPhDescend : kPhTlVisit;
         continue;
       }
       // ---- Traversal Verification ----------------------------------------
       case kPhDescend: {   // walk to the first leaf of the remaining tree
-        const int j = sm.cur;
+        const int j = ct.cur;
         if (sm.next_child[j] < sm.child_count[j]) {
           if (sm.pi[j] > 0.0) {
             if (!(sm.flags[j] & kFlagConsulted)) {
               sm.flags[j] |= kFlagConsulted;
-              ++sm.rows_consulted;
+              ++ct.rows;
             }
             if (!(sm.flags[j] & kFlagStats)) { issue_stats(sm, j, true, true); return; }
+            if (sm.flags[j] & kFlagBad) { fail(sm, TV_TREE_NONFINITE); return; }
           }
           const int c = sm.child_list[sm.child_start[j] + sm.next_child[j]];
           init_node_state(sm, c, child_rate(sm, P.mode, j, c));
-          sm.cur = c;
+          ct.cur = c;
           continue;
         }
-        sm.phase = kPhTest;
+        ct.phase = kPhTest;
         continue;
       }
       case kPhTest: {
-        const int l = sm.cur;
+        const int l = ct.cur;
         if (l == 0) {                       // only the root is left: p(X_0) = 1
-          sm.accepted = 0;
+          ct.accepted = 0;
           sm.state[0] = TV_NODE_ACCEPTED;
-          sm.phase = kPhFinal;
+          ct.phase = kPhFinal;
           continue;
         }
         const int j = sm.parent[l];
@@ -852,38 +948,38 @@ __device__ __attribute__((noinline)) void advance(TreeSmem& sm, const Params& P,
           sm.state[l] = TV_NODE_PRUNED;
           sm.theta[l] = 0.0f;
           ++sm.next_child[j];
-          sm.cur = j;
-          sm.phase = kPhDescend;
+          ct.cur = j;
+          ct.phase = kPhDescend;
           continue;
         }
         const double th = sm.pi[l];
         sm.theta[l] = static_cast<float>(th);
-        ++sm.tests;
+        ++ct.tests;
         if (static_cast<double>(sm.u[l]) < th) {
           sm.state[l] = TV_NODE_ACCEPTED;
-          sm.accepted = l;
-          sm.phase = kPhFinal;
+          ct.accepted = l;
+          ct.phase = kPhFinal;
           continue;
         }
         sm.state[l] = TV_NODE_REJECTED;
         ++sm.next_child[j];
         const double cc = wo ? 1.0 / sm.rem[j] : 1.0;
-        sm.alpha = sm.pi[j] * sm.A[j];
-        sm.beta = sm.pi[j] * sm.B[j] + cc;
-        sm.rejected = l;
-        sm.phase = kPhAfterSPass;
-        issue_spass(sm, j, sm.alpha, sm.beta, wo);
+        ct.alpha = sm.pi[j] * sm.A[j];
+        ct.beta = sm.pi[j] * sm.B[j] + cc;
+        ct.rejected = l;
+        ct.phase = kPhAfterSPass;
+        issue_spass(sm, j, ct.alpha, ct.beta, wo, true);
         return;
       }
       case kPhAfterSPass: {                 // Eq. (e1), (e2), (e3) at the parent
-        const int l = sm.rejected;
+        const int l = ct.rejected;
         const int j = sm.parent[l];
         const double S = sm.res_S;
-        ++sm.resid_passes;
+        ++ct.resid;
         if (S > 0.0) {
           const double inv = 1.0 / S;
-          sm.A[j] = sm.alpha * inv;
-          sm.B[j] = sm.beta * inv;
+          sm.A[j] = ct.alpha * inv;
+          sm.B[j] = ct.beta * inv;
           sm.pi[j] = S / (S + (1.0 - sm.pi[j]));
         } else if (j == 0) {
           fail(sm, TV_TREE_DEGENERATE);
@@ -891,79 +987,96 @@ __device__ __attribute__((noinline)) void advance(TreeSmem& sm, const Params& P,
         } else {
           sm.pi[j] = 0.0;
         }
-        if (wo) update_remaining_mass(sm, j);
-        sm.cur = j;
-        sm.phase = kPhDescend;
+        if (wo) update_remaining_mass(sm, j, summed_draft);
+        ct.cur = j;
+        ct.phase = kPhDescend;
         continue;
       }
       // ---- Token-level verification --------------------------------------
       case kPhTlVisit: {
-        const int j = sm.cur;
+        const int j = ct.cur;
         if (sm.child_count[j] == 0) {       // accepted leaf: Y from its target row
-          sm.accepted = j;
+          ct.accepted = j;
           if (j == 0) sm.state[0] = TV_NODE_ACCEPTED;
-          sm.phase = kPhFinal;
+          ct.phase = kPhFinal;
           continue;
         }
         if (!(sm.flags[j] & kFlagConsulted)) {
           sm.flags[j] |= kFlagConsulted;
-          ++sm.rows_consulted;
+          ++ct.rows;
         }
-        if (!(sm.flags[j] & kFlagStats)) { issue_stats(sm, j, true, true); return; }
+        if (!(sm.flags[j] & kFlagStats)) { issue_stats(sm, j, true, false); return; }
+        if (sm.flags[j] & kFlagBad) { fail(sm, TV_TREE_NONFINITE); return; }
         if (sm.next_child[j] == sm.child_count[j]) {   // all rejected: Y from residual
-          sm.accepted = j;
+          ct.accepted = j;
           if (j == 0) sm.state[0] = TV_NODE_ACCEPTED;
-          sm.phase = kPhFinal;
+          ct.phase = kPhFinal;
           continue;
         }
         const int c = sm.child_list[sm.child_start[j] + sm.next_child[j]];
         const double th = child_rate(sm, P.mode, j, c);
         sm.theta[c] = static_cast<float>(th);
-        ++sm.tests;
+        ++ct.tests;
         if (static_cast<double>(sm.u[c]) < th) {
           sm.state[c] = TV_NODE_ACCEPTED;
           init_node_state(sm, c, 1.0);
-          sm.cur = c;
+          ct.cur = c;
           continue;
         }
         sm.state[c] = TV_NODE_REJECTED;
         ++sm.next_child[j];
         const double cc = wo ? 1.0 / sm.rem[j] : 1.0;
-        sm.alpha = sm.A[j];
-        sm.beta = sm.B[j] + cc;
-        sm.rejected = c;
-        sm.phase = kPhTlAfterSPass;
-        issue_spass(sm, j, sm.alpha, sm.beta, wo);
+        ct.alpha = sm.A[j];
+        ct.beta = sm.B[j] + cc;
+        ct.rejected = c;
+        ct.phase = kPhTlAfterSPass;
+        issue_spass(sm, j, ct.alpha, ct.beta, wo, false);
         return;
       }
       case kPhTlAfterSPass: {               // Algorithm 2 rejection branch
-        const int c = sm.rejected;
+        const int c = ct.rejected;
         const int j = sm.parent[c];
         const double S = sm.res_S;
-        ++sm.resid_passes;
+        ++ct.resid;
         if (!(S > 0.0)) { fail(sm, TV_TREE_DEGENERATE); return; }
         const double inv = 1.0 / S;
-        sm.A[j] = sm.alpha * inv;
-        sm.B[j] = sm.beta * inv;
-        if (wo) update_remaining_mass(sm, j);
-        sm.phase = kPhTlVisit;
+        sm.A[j] = ct.alpha * inv;
+        sm.B[j] = ct.beta * inv;
+        if (wo) update_remaining_mass(sm, j, summed_draft);
+        ct.phase = kPhTlVisit;
         continue;
       }
       // ---- Final sample Y --------------------------------------------------
       case kPhFinal: {
-        const int a = sm.accepted;
-        if (sm.child_count[a] == 0) {
-          sm.phase = kPhFinalLeafStats;
-          if (!(sm.flags[a] & kFlagLeafStats)) { issue_stats(sm, a, false, false); return; }
-          continue;
+        const int a = ct.accepted;
+        if (sm.child_count[a] == 0) {       // accepted leaf: its target row
+          ct.phase = kPhFinalLeafStats;
+          issue_stats(sm, a, false, false);
+          return;
         }
-        sm.phase = kPhAfterSample;
-        issue_sample(sm, a, false);
+        if (sm.spass_node == a) {           // weights of the SPASS just done at a
+          ct.phase = kPhAfterSample;
+          request_sample(sm, false, true, sm.last_ap, sm.last_bp, sm.last_cb, sm.last_cs);
+          return;
+        }
+        ct.phase = kPhFinalWSum;            // residual weights need a pass of their own
+        batch_begin(sm, kCmdWSum, a);
+        sm.cmd_ap = sm.A[a] * sm.invsb[a];
+        sm.cmd_bp = sm.B[a] * sm.invss[a];
+        sm.cmd_cb = sm.cb[a];
+        sm.cmd_cs = sm.cs[a];
         return;
       }
       case kPhFinalLeafStats: {
-        sm.phase = kPhAfterSample;
-        issue_sample(sm, sm.accepted, true);
+        const int a = ct.accepted;
+        if (sm.flags[a] & kFlagBad) { fail(sm, TV_TREE_NONFINITE); return; }
+        ct.phase = kPhAfterSample;
+        request_sample(sm, true, false, 1.0, 0.0, sm.cb[a], 0.0);
+        return;
+      }
+      case kPhFinalWSum: {
+        ct.phase = kPhAfterSample;
+        request_sample(sm, false, true, sm.last_ap, sm.last_bp, sm.last_cb, sm.last_cs);
         return;
       }
       case kPhAfterSample: {
@@ -978,29 +1091,48 @@ __device__ __attribute__((noinline)) void advance(TreeSmem& sm, const Params& P,
   }
 }
 
+// The controller's scalars live in registers for the duration of a step.
+template <int kCap>
+__device__ __attribute__((always_inline)) void advance(Lds<TreeSmem<kCap>>& sm, TraversalArgs P,
+                                                      int done_cmd) {
+  Ctl ct{sm.phase, sm.cur, sm.accepted, sm.rejected, sm.rows_consulted, sm.resid_passes,
+         sm.tests, sm.pinit_next, sm.alpha, sm.beta};
+  advance_impl(sm, P, done_cmd, ct);
+  sm.phase = ct.phase;
+  sm.cur = ct.cur;
+  sm.accepted = ct.accepted;
+  sm.rejected = ct.rejected;
+  sm.rows_consulted = ct.rows;
+  sm.resid_passes = ct.resid;
+  sm.tests = ct.tests;
+  sm.pinit_next = ct.pinit_next;
+  sm.alpha = ct.alpha;
+  sm.beta = ct.beta;
+}
+
 // ---------------------------------------------------------------------------
-// The kernel: one workgroup per tree
+// Owner: tree set-up, combining a completed batch, local sample, publishing
 // ---------------------------------------------------------------------------
 
-template <typename T, class A, int algo>
-__global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
-  __shared__ TreeSmem sm;
+template <typename T, class PP>
+__device__ __forceinline__ const T* row_ptr(const PP& P, const void* base, int b, int node) {
+  return static_cast<const T*>(base) +
+         (static_cast<size_t>(b) * P.num_nodes + node) * static_cast<size_t>(P.vocab);
+}
+
+// Loads and checks tree b into LDS, gathers every node's logits at its token
+// in its parent's rows, and starts the traversal (all threads).
+template <typename T, int kCap>
+__device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, const Lds<Params>& P,
+                                                     int b) {
   const int tid = threadIdx.x;
-  const int b = blockIdx.x;
   const int n1 = P.num_nodes;
   const int V = P.vocab;
   const size_t tree_off = static_cast<size_t>(b) * n1;
-  const T* zb = static_cast<const T*>(P.target) + tree_off * V;
-  const T* zs = static_cast<const T*>(P.draft) + tree_off * V;
-
-  // ---- load and check the tree -----------------------------------------
-  if (tid == 0) {
-    sm.status = TV_TREE_OK;
-    sm.res_bad = 0;
-  }
+  if (tid == 0) sm.status = TV_TREE_OK;
   __syncthreads();
   int bad_parent = 0, bad_token = 0;
-  for (int i = tid; i < n1; i += kThreads) {
+  for (int i = tid; i < n1; i += kNT) {
     const int p = P.parents[tree_off + i];
     const int x = P.tokens[tree_off + i];
     if (i == 0 ? p != -1 : (p < 0 || p >= i)) bad_parent = 1;
@@ -1023,7 +1155,9 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
   }
   __syncthreads();
   if (sm.status == TV_TREE_OK) {
-    for (int i = 1 + tid; i < n1; i += kThreads) atomicAdd(&sm.child_count[sm.parent[i]], 1);
+    for (int i = 1 + tid; i < n1; i += kNT)
+      __hip_atomic_fetch_add(&sm.child_count[sm.parent[i]], 1, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_WORKGROUP);
     __syncthreads();
     if (tid == 0) {
       int start = 0;
@@ -1034,7 +1168,7 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
     }
     __syncthreads();
     // rank among siblings = earlier nodes with the same parent
-    for (int i = 1 + tid; i < n1; i += kThreads) {
+    for (int i = 1 + tid; i < n1; i += kNT) {
       const int p = sm.parent[i];
       int rank = 0, d = 1;
       for (int k2 = 1; k2 < i; ++k2) rank += (sm.parent[k2] == p);
@@ -1046,7 +1180,7 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
     __syncthreads();
     int dup = 0;
     if (P.mode == TV_SIBLINGS_WITHOUT_REPLACEMENT) {
-      for (int i = 1 + tid; i < n1; i += kThreads) {
+      for (int i = 1 + tid; i < n1; i += kNT) {
         const int p = sm.parent[i];
         const int s0 = sm.child_start[p], cnt = sm.child_count[p];
         for (int r = 0; r < cnt; ++r) {
@@ -1057,55 +1191,41 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
     }
     dup = __syncthreads_or(dup);
     if (tid == 0 && dup) sm.status = TV_TREE_DUP_SIBLING;
-    __syncthreads();
-  }
-
-  // ---- traversal ---------------------------------------------------------
-  if (sm.status == TV_TREE_OK) {
-    if (tid == 0) {
-      sm.algo = algo;
-      sm.cur = 0;
-      sm.accepted = -1;
-      sm.rows_consulted = sm.resid_passes = sm.tests = 0;
-      sm.pinit_next = 0;
-      init_node_state(sm, 0, 1.0);
-      sm.res_y = -1;
-      sm.cmd = -1;
-      sm.cmd_sd = 0;
-      if (P.p_init && algo == static_cast<int>(tv::Algo::kTraversal)) sm.phase = kPhPinit;
-      else if (algo == static_cast<int>(tv::Algo::kTraversal)) sm.phase = kPhDescend;
-      else sm.phase = kPhTlVisit;
-      advance(sm, P, ar);
-    }
-    __syncthreads();
-    for (;;) {
-      const int cmd = sm.cmd;
-      if (cmd == kCmdDone) break;
-      const int node = sm.cmd_node;
-      const T* rb = zb + static_cast<size_t>(node) * V;
-      const T* rs = zs + static_cast<size_t>(node) * V;
-      if (cmd == kCmdStats) {
-        if (sm.cmd_two_rows) stats_pass<T, A, true>(sm, rb, rs, V, ar, node, sm.cmd_gather != 0);
-        else stats_pass<T, A, false>(sm, rb, rs, V, ar, node, false);
-      } else {
-        const TermParams tp{sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp};
-        if (cmd == kCmdSPass) {
-          if (sm.cmd_sd) s_pass<T, A, true>(sm, rb, rs, V, ar, tp);
-          else s_pass<T, A, false>(sm, rb, rs, V, ar, tp);
-        } else if (sm.cmd_two_rows) {
-          sample_pass<T, A, true>(sm, rb, rs, V, ar, tp, sm.u[0]);
-        } else {
-          sample_pass<T, A, false>(sm, rb, rs, V, ar, tp, sm.u[0]);
-        }
-      }
-      if (tid == 0) advance(sm, P, ar);
-      __syncthreads();
+    for (int i = 1 + tid; i < n1; i += kNT) {
+      const int j = sm.parent[i], x = sm.token[i];
+      sm.gb[i] = Elem<T>::scalar(row_ptr<T>(P, P.target, b, j) + x);
+      sm.gs[i] = Elem<T>::scalar(row_ptr<T>(P, P.draft, b, j) + x);
     }
   }
+  if (tid == 0) {
+    sm.has_tree = 1;
+    sm.tree = b;
+    sm.cur = 0;
+    sm.accepted = -1;
+    sm.rows_consulted = sm.resid_passes = sm.tests = 0;
+    sm.pinit_next = 0;
+    init_node_state(sm, 0, 1.0);
+    sm.res_y = -1;
+    sm.cmd = kCmdNone;
+    sm.pending = 0;
+    sm.spass_node = -1;
+    const bool tv_algo = P.algo == static_cast<int>(tv::Algo::kTraversal);
+    if (P.p_init && tv_algo) sm.phase = kPhPinit;
+    else sm.phase = tv_algo ? kPhDescend : kPhTlVisit;
+  }
+  __syncthreads();
+}
 
-  // ---- outputs -------------------------------------------------------------
+// Writes the tree's outputs (all threads) and retires it.
+template <int kCap>
+__device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& sm,
+                                                           const Lds<Params>& P) {
+  const int tid = threadIdx.x;
+  const int b = sm.tree;
+  const int n1 = P.num_nodes;
+  const size_t tree_off = static_cast<size_t>(b) * n1;
   const bool ok = sm.status == TV_TREE_OK;
-  for (int i = tid; i < n1; i += kThreads) {
+  for (int i = tid; i < n1; i += kNT) {
     if (P.node_state) P.node_state[tree_off + i] = ok ? static_cast<int8_t>(sm.state[i]) : 0;
     if (P.node_theta) P.node_theta[tree_off + i] = ok ? sm.theta[i] : -1.0f;
     if (P.p_init) P.p_init[tree_off + i] = ok ? static_cast<float>(sm.pini[i]) : -1.0f;
@@ -1122,6 +1242,554 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
       c[2] = ok ? (sm.child_count[sm.accepted] == 0 ? 1 : 0) : 0;
       c[3] = ok ? sm.tests : 0;
     }
+    // withdraw the offer (nothing left to claim) and retire the tree
+    st_rlx(&ws_words(P)[blockIdx.x], 0ull);
+    __hip_atomic_fetch_sub(ws_remaining(P), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sm.has_tree = 0;
+  }
+  __syncthreads();
+}
+
+// Publishes the batch the controller asked for (thread 0).
+template <typename T, int kCap>
+__device__ __attribute__((always_inline)) void publish(Lds<TreeSmem<kCap>>& sm,
+                                                       const Lds<Params>& P) {
+  if (threadIdx.x == 0) {
+    const int b = sm.tree;
+    const int bn = sm.bn;
+    int nseg = 1;
+    uint64_t nodes[2] = {0, 0}, cmds = 0;
+    for (int p = 0; p < bn; ++p) {
+      const int node = sm.bnode[p];
+      nseg = max(nseg, num_segments(row_geom(row_ptr<T>(P, P.target, b, node), P.vocab)));
+      nodes[p >> 2] |= static_cast<uint64_t>(node) << (16 * (p & 3));
+      cmds |= static_cast<uint64_t>(sm.bcmd[p]) << (4 * p);
+    }
+    const uint32_t seq = ++sm.seq;
+    uint64_t d[kDescWords] = {
+        static_cast<uint64_t>(__double_as_longlong(sm.cmd_ap)),
+        static_cast<uint64_t>(__double_as_longlong(sm.cmd_bp)),
+        static_cast<uint64_t>(__double_as_longlong(sm.cmd_cb)),
+        static_cast<uint64_t>(__double_as_longlong(sm.cmd_cs)),
+        nodes[0], nodes[1], cmds, seq};
+    uint64_t* g = ws_desc(P, blockIdx.x);
+    for (int i = 0; i < kDescWords; ++i) {
+      sm.desc[i] = d[i];
+      st_rlx(g + i, d[i]);
+    }
+    const int cmd0 = sm.bcmd[0];
+    sm.pending = 1;
+    sm.bnseg = nseg;
+    sm.last_ap = sm.cmd_ap;
+    sm.last_bp = sm.cmd_bp;
+    sm.last_cb = sm.cmd_cb;
+    sm.last_cs = sm.cmd_cs;
+    sm.spass_node = (cmd0 == kCmdSPass || cmd0 == kCmdSPassSd) ? sm.bnode[0] : -1;
+    sm.expect_done += static_cast<uint32_t>(bn * nseg);
+    stores_done();
+    st_rlx(&ws_words(P)[blockIdx.x], pack_work(bn * nseg, nseg, b, static_cast<int>(seq)));
+  }
+  __syncthreads();
+}
+
+// Combines the segment partials of the completed batch (all threads): wave w
+// takes passes w, w + 4; STATS results go to the node arrays, a SPASS / WSUM
+// result to res_S / res_sd.
+template <typename T, class A, int kCap>
+__device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
+                                                       const Lds<Params>& P, A ar) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bn = sm.bn;
+  const int nseg = sm.bnseg;
+  fence_acquire();
+  for (int p = wave; p < bn; p += kNW) {
+    const int cmd = sm.bcmd[p];
+    const int node = sm.bnode[p];
+    const SegPart* part = ws_parts(P, blockIdx.x, p);
+    double s0 = 0.0, s1 = 0.0;
+    float m0 = -INFINITY, m1 = -INFINITY;
+    if (lane < nseg) {
+      s0 = ld_rlx_f64(&part[lane].s0);
+      s1 = ld_rlx_f64(&part[lane].s1);
+      const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
+      m0 = __uint_as_float(static_cast<uint32_t>(mm));
+      m1 = __uint_as_float(static_cast<uint32_t>(mm >> 32));
+    }
+    if (cmd == kCmdStats2 || cmd == kCmdStats1) {
+      const bool two = cmd == kCmdStats2;
+      const float Mb = wave_max(m0);
+      const float Ms = two ? wave_max(m1) : -INFINITY;
+      const double Cb = ar.frame(Mb);
+      const double Cs = two ? ar.frame(Ms) : 0.0;
+      // segment sums in the row's frame; a segment with no finite value adds 0 (or NaN)
+      double tb = (m0 > -INFINITY) ? s0 * exp2(Cb - ar.frame(m0)) : s0;
+      double ts = two ? ((m1 > -INFINITY) ? s1 * exp2(Cs - ar.frame(m1)) : s1) : 0.0;
+      tb = __shfl(wave_sum(tb), 0, 64);
+      ts = __shfl(wave_sum(ts), 0, 64);
+      if (lane == 0) {
+        const bool bad = !(Mb > -INFINITY) || !isfinite(tb) ||
+                         (two && (!(Ms > -INFINITY) || !isfinite(ts)));
+        sm.cb[node] = Cb;
+        sm.invsb[node] = 1.0 / tb;
+        if (two) {
+          sm.cs[node] = Cs;
+          sm.invss[node] = 1.0 / ts;
+        }
+        sm.flags[node] |= kFlagStats | (bad ? kFlagBad : 0);
+      }
+    } else {
+      const double S = __shfl(wave_sum(s0), 0, 64);
+      const double sd = __shfl(wave_sum(s1), 0, 64);
+      if (lane == 0) {
+        sm.res_S = S;
+        sm.res_sd = sd;
+      }
+    }
+  }
+  __syncthreads();
+  // children's original ratios r0 = p(x)/q(x) and draft terms
+  const double kd = ar.kd();
+  for (int p = 0; p < bn; ++p) {
+    const int node = sm.bnode[p];
+    if (sm.bcmd[p] != kCmdStats2 || (sm.flags[node] & kFlagBad)) continue;
+    const double Cb = sm.cb[node], Cs = sm.cs[node];
+    const double lsb = -log2(sm.invsb[node]), lss = -log2(sm.invss[node]);
+    for (int i = tid; i < sm.child_count[node]; i += kNT) {
+      const int c = sm.child_list[sm.child_start[node] + i];
+      const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb) - lsb;
+      const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs) - lss;
+      sm.r0[c] = exp2(lp - lq);
+      sm.et[c] = ar.ex(sm.gs[c], Cs);
+      if (sm.gs[c] == -INFINITY) sm.flags[node] |= kFlagBad;   // a token the draft cannot produce
+    }
+  }
+  __syncthreads();
+}
+
+// Inverse-CDF draw of Y (all threads). The weights of the segments come from the
+// partials of pass 0 of the batch just completed; the segment holding u*W is
+// rescanned.
+template <typename T, class A, int kCap>
+__device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
+                                                       const Lds<Params>& P, A ar) {
+  constexpr int E = Elem<T>::E;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int node = sm.bnode[0];
+  const int nseg = sm.bnseg;
+  if (tid < 64) {
+    const SegPart* part = ws_parts(P, blockIdx.x, 0);
+    double w = 0.0;
+    if (lane < nseg) {
+      const double s0 = ld_rlx_f64(&part[lane].s0);
+      if (sm.smp_from_stats) {
+        const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
+        const float m0 = __uint_as_float(static_cast<uint32_t>(mm));
+        w = (m0 > -INFINITY) ? s0 * exp2(sm.smp_cb - ar.frame(m0)) : 0.0;
+      } else {
+        w = s0;
+      }
+    }
+    double incl = w;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const double o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
+    }
+    const double W = __shfl(incl, nseg - 1, 64);
+    const double target = static_cast<double>(sm.u[0]) * W;
+    const uint64_t pos = __ballot(lane < nseg && w > 0.0);
+    const uint64_t hits = __ballot(lane < nseg && w > 0.0 && target < incl);
+    int seg = -1;
+    bool fallback = false;
+    if (W > 0.0 && isfinite(W) && pos != 0) {
+      if (hits) {
+        seg = __ffsll(static_cast<long long>(hits)) - 1;
+      } else {                              // rounding at the end: last segment with mass
+        seg = 63 - __clzll(static_cast<long long>(pos));
+        fallback = true;
+      }
+    }
+    if (lane == 0) ws.smp_seg = seg;
+    if (seg >= 0 && lane == seg) ws.smp_target = fallback ? INFINITY : target - (incl - w);
+  }
+  if (tid == 0) {
+    ws.hit = kNT;
+    ws.last_pos = -1;
+    sm.res_y = -2;
+  }
+  __syncthreads();
+  const int seg = ws.smp_seg;
+  if (seg < 0) return;     // no mass: res_y stays negative (degenerate)
+  const double local = ws.smp_target;
+  const T* rb = row_ptr<T>(P, P.target, sm.tree, node);
+  const T* rs = row_ptr<T>(P, P.draft, sm.tree, node);
+  const Geom g = row_geom(rb, P.vocab);
+  const SegRange r = seg_range(g, seg, num_segments(g));
+  const int nh = r.first ? g.head : 0;
+  const int nv = max(0, r.ve - r.vb);
+  const int nt = r.last ? g.tail : 0;
+  const int nu = nh + nv + nt;
+  const int u0 = static_cast<int>((static_cast<long long>(tid) * nu) / kNT);
+  const int u1 = static_cast<int>((static_cast<long long>(tid + 1) * nu) / kNT);
+  const TermParams tp{sm.smp_cb, sm.smp_cs, sm.smp_ap, sm.smp_bp};
+  const int tail0 = g.head + g.nvec * E;
+  auto run = [&](auto two_tag) {
+    constexpr bool TWO = decltype(two_tag)::value;
+    using TM = Terms<A, TWO, false>;
+    const TM tm(ar, tp);
+    double unused = 0.0;
+    // element weights of unit i of the segment (a head/tail element or a
+    // vector); returns the count and the first token id
+    auto unit = [&](int i, double (&wd)[E], int& tok0) -> int {
+      if (i < nh || i >= nh + nv) {
+        const int x = i < nh ? i : tail0 + (i - nh - nv);
+        wd[0] = scalar_weight<T, TM, TWO>(tm, rb, rs, x, unused);
+        tok0 = x;
+        return 1;
+      }
+      const int v = r.vb + (i - nh);
+      float xb[E], xs[E];
+      Elem<T>::unpack(load16(rb, g.head, v), xb);
+      if constexpr (TWO) {
+        Elem<T>::unpack(load16(rs, g.head, v), xs);
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) xs[e] = 0.0f;
+      }
+      typename TM::W w[E];
+      tm.weights(xb, xs, w, unused);
+#pragma unroll
+      for (int e = 0; e < E; ++e) wd[e] = static_cast<double>(w[e]);
+      tok0 = g.head + v * E;
+      return E;
+    };
+    // the same unit sums as the pass: fp32 (fast) or fp64 (precise) per unit
+    auto unit_sum = [&](int i) -> double {
+      if (i < nh || i >= nh + nv) {
+        const int x = i < nh ? i : tail0 + (i - nh - nv);
+        return scalar_weight<T, TM, TWO>(tm, rb, rs, x, unused);
+      }
+      const int v = r.vb + (i - nh);
+      const uint4 vb = load16(rb, g.head, v);
+      const uint4 vs = TWO ? load16(rs, g.head, v) : make_uint4(0, 0, 0, 0);
+      return vec_sum<T, TM, TWO>(tm, vb, vs, unused);
+    };
+    double mine = 0.0;
+    for (int i = u0; i < u1; ++i) mine += unit_sum(i);
+    const double incl = block_incl_scan(ws, mine);
+    const double excl = incl - mine;
+    if (mine > 0.0) {
+      if (local < incl)
+        __hip_atomic_fetch_min(&ws.hit, tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      __hip_atomic_fetch_max(&ws.last_pos, tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    __syncthreads();
+    const bool fallback = ws.hit >= kNT;
+    const int chosen = fallback ? ws.last_pos : ws.hit;
+    if (tid == chosen) {
+      double C = excl;
+      int y = -1, last = -1;
+      for (int i = u0; i < u1 && y < 0; ++i) {
+        const double us = unit_sum(i);
+        double wd[E];
+        int tok0 = 0;
+        const int n = unit(i, wd, tok0);
+        if (!fallback && us > 0.0 && local < C + us) {
+          double C2 = C;
+          for (int e = 0; e < n; ++e) {
+            if (wd[e] > 0.0) {
+              last = tok0 + e;
+              if (local < C2 + wd[e]) { y = tok0 + e; break; }
+            }
+            C2 += wd[e];
+          }
+          if (y < 0) y = last;         // rounding inside the unit: its last positive weight
+        } else {
+          for (int e = 0; e < n; ++e)
+            if (wd[e] > 0.0) last = tok0 + e;
+        }
+        C += us;
+      }
+      if (y < 0) y = last;             // rounding at the end: last positive weight
+      sm.res_y = y;
+    }
+  };
+  if (sm.smp_two) run(std::true_type{});
+  else run(std::false_type{});
+  __syncthreads();
+}
+
+// One controller step of the owner (all threads): combine the completed batch,
+// advance the traversal, then publish the next batch or finish the tree.
+template <typename T, class A, int kCap>
+__device__ __attribute__((noinline)) void owner_step(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
+                                                     const Lds<Params>& P, A ar) {
+  const int tid = threadIdx.x;
+  if (sm.status == TV_TREE_OK) {
+    int done_cmd = kCmdNone;
+    if (sm.pending) {
+      combine<T, A>(sm, P, ar);
+      done_cmd = sm.bcmd[0];
+      if (tid == 0) sm.pending = 0;
+    }
+    for (;;) {
+      if (tid == 0) advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
+      __syncthreads();
+      if (sm.cmd != kCmdLocalSample) break;
+      local_sample<T, A>(sm, ws, P, ar);
+      done_cmd = kCmdLocalSample;
+    }
+  } else if (tid == 0) {
+    sm.cmd = kCmdDone;
+  }
+  __syncthreads();
+  if (sm.cmd == kCmdDone) {
+    finish_tree(sm, P);
+    return;
+  }
+  publish<T>(sm, P);
+}
+
+// Claims item `old` of owner slot o's batch if it is valid; the descriptor
+// words were loaded alongside the claim and are reloaded if they belong to an
+// earlier batch. Wavefront 0.
+template <class PP>
+__device__ __forceinline__ bool take_item(Lds<WgScratch>& ws, const PP& P, int o, uint64_t old,
+                                          uint64_t dword, long long t0) {
+  const int lane = threadIdx.x & 63;
+  const Work got = unpack_work(old);
+  if (got.cnt >= got.total) return false;
+  fence_acquire();
+  const uint64_t* g = ws_desc(P, o);
+  for (;;) {
+    const uint64_t seq = __shfl(static_cast<int>(dword & 0x3FFFu), kDescWords - 1, 64);
+    if (static_cast<int>(seq) == got.seq) break;
+    if (lane < kDescWords) dword = ld_rlx(g + lane);
+    if (wall_clock64() - t0 > P.spin_limit) break;
+  }
+  if (lane < kDescWords) ws.item_desc[lane] = dword;
+  if (lane == 0) {
+    ws.item_owner = o;
+    ws.item_word = old;
+  }
+  return true;
+}
+
+// Wavefront 0: waits until this workgroup's batch is complete, it claims a
+// tree or an item of some published batch, or the launch is over.
+template <int kCap>
+__device__ int wait_event(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws, const Params& P) {
+  const int lane = threadIdx.x & 63;
+  const int self = blockIdx.x;
+  const int grid = P.grid;
+  uint64_t* words = ws_words(P);
+  long long t0 = wall_clock64();
+  uint32_t last_rem = 0xFFFFFFFFu;
+  const int rot = (self * 37) & 63;
+  int backoff = 0;
+  for (;;) {
+    if (sm.has_tree) {
+      // An owner works on its own batch only, so that it sees the batch
+      // complete as soon as possible: claim its items, then wait.
+      if (!sm.pending) return kEvOwn;
+      uint64_t old = 0;
+      uint32_t d = 0;
+      if (lane == 0) {
+        const Work wk = unpack_work(ld_rlx(&words[self]));
+        if (wk.cnt < wk.total)
+          old = __hip_atomic_fetch_add(&words[self], 1ull, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+        else
+          d = ld_rlx(&ws_done(P)[self]);
+      }
+      old = shfl_u64(old, 0);
+      d = __shfl(d, 0, 64);
+      const uint64_t dword = lane < kDescWords ? sm.desc[lane] : 0ull;
+      if (old != 0 && take_item(ws, P, self, old, dword, t0)) return kEvItem;
+      if (old == 0 && static_cast<int32_t>(d - sm.expect_done) >= 0) return kEvOwn;
+      if (wall_clock64() - t0 > P.spin_limit) {
+        if (lane == 0) st_rlx(ws_abort(P), 1u);
+        return kEvExit;
+      }
+      continue;
+    }
+    if (ws.trees_left) {
+      uint32_t t = 0;
+      if (lane == 0)
+        t = __hip_atomic_fetch_add(ws_next_tree(P), 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+      t = __shfl(t, 0, 64);
+      if (t < static_cast<uint32_t>(P.batch)) {
+        if (lane == 0) ws.new_tree = static_cast<int>(t);
+        return kEvTree;
+      }
+      if (lane == 0) ws.trees_left = 0;
+    }
+    // scan the work words, 64 at a time from a rotating start
+    bool raced = false;
+    const int start = ws.scan_pos;
+    for (int base = 0; base < grid; base += 64) {
+      const int idx = base + lane;
+      int o = start + idx;
+      if (o >= grid) o -= grid;
+      uint64_t w = 0;
+      if (idx < grid) w = ld_rlx(&words[o]);
+      const Work wk = unpack_work(w);
+      const uint64_t avail = __ballot(idx < grid && wk.cnt < wk.total);
+      if (!avail) continue;
+      // one candidate: the k-th available word, k spread by workgroup index, so
+      // that idle workgroups do not all race for the same item
+      const int navail = __popcll(avail);
+      const int k = (self + rot) % navail;
+      const int below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(avail >> 32),
+                                                  __builtin_amdgcn_mbcnt_lo(
+                                                      static_cast<uint32_t>(avail), 0u));
+      const uint64_t pick = __ballot(((avail >> lane) & 1ull) && below == k);
+      const int l = __ffsll(static_cast<long long>(pick)) - 1;
+      const int oc = __shfl(o, l, 64);
+      // the claim and the descriptor loads go out together
+      uint64_t old = 0, dword = 0;
+      if (lane == 0)
+        old = __hip_atomic_fetch_add(&words[oc], 1ull, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+      else if (lane <= kDescWords)
+        dword = ld_rlx(ws_desc(P, oc) + (lane - 1));
+      old = shfl_u64(old, 0);
+      dword = shfl_u64(dword, (lane + 1) & 63);    // lane i holds word i
+      if (take_item(ws, P, oc, old, dword, t0)) {
+        if (lane == 0) ws.scan_pos = oc;
+        return kEvItem;
+      }
+      raced = true;       // another workgroup took the last item: look again
+      break;
+    }
+    if (raced) continue;
+    uint32_t rem = 0, ab = 0;
+    if (lane == 0) {
+      rem = ld_rlx(ws_remaining(P));
+      ab = ld_rlx(ws_abort(P));
+    }
+    rem = __shfl(rem, 0, 64);
+    ab = __shfl(ab, 0, 64);
+    if (rem == 0 || ab) return kEvExit;
+    const long long now = wall_clock64();
+    if (rem != last_rem) {            // trees are being finished: progress
+      last_rem = rem;
+      t0 = now;
+    } else if (now - t0 > P.spin_limit) {
+      if (lane == 0) st_rlx(ws_abort(P), 1u);
+      return kEvExit;
+    }
+    if (backoff < 8) ++backoff;
+    for (int s = 0; s < backoff; ++s) __builtin_amdgcn_s_sleep(8);
+  }
+}
+
+// A claimed item (all threads): compute its segment's partial result and
+// report it.
+template <typename T, class A>
+__device__ void run_segment(Lds<WgScratch>& ws, const Params& P, const A& ar) {
+  const int o = ws.item_owner;
+  const Work wk = unpack_work(ws.item_word);
+  uint64_t d[kDescWords];
+#pragma unroll
+  for (int i = 0; i < kDescWords; ++i) d[i] = ws.item_desc[i];
+  const int pass = wk.cnt / wk.nseg;
+  const int seg = wk.cnt - pass * wk.nseg;
+  const int node = desc_node(d, pass);
+  const int cmd = desc_cmd(d, pass);
+  const T* rb = row_ptr<T>(P, P.target, wk.tree, node);
+  const T* rs = row_ptr<T>(P, P.draft, wk.tree, node);
+  const Geom g = row_geom(rb, P.vocab);
+  // rows of a batch can differ by one segment (alignment); beyond its last
+  // segment a row contributes an empty partial
+  const SegRange r = seg_range(g, seg, num_segments(g));
+  SegPart part;
+  switch (cmd) {
+    case kCmdStats2: seg_stats<T, A, true>(ws, rb, rs, g, r, ar, part); break;
+    case kCmdStats1: seg_stats<T, A, false>(ws, rb, rs, g, r, ar, part); break;
+    default: {
+      const TermParams tp{__longlong_as_double(static_cast<long long>(d[2])),
+                          __longlong_as_double(static_cast<long long>(d[3])),
+                          __longlong_as_double(static_cast<long long>(d[0])),
+                          __longlong_as_double(static_cast<long long>(d[1]))};
+      if (cmd == kCmdSPassSd) seg_wsum<T, A, true>(ws, rb, rs, g, r, ar, tp, part);
+      else seg_wsum<T, A, false>(ws, rb, rs, g, r, ar, tp, part);
+      break;
+    }
+  }
+  if (threadIdx.x == 0) {
+    SegPart* dst = ws_parts(P, o, pass) + seg;
+    st_rlx_f64(&dst->s0, part.s0);
+    st_rlx_f64(&dst->s1, part.s1);
+    st_rlx(reinterpret_cast<uint64_t*>(&dst->m0),
+           (static_cast<uint64_t>(__float_as_uint(part.m1)) << 32) | __float_as_uint(part.m0));
+    stores_done();
+    __hip_atomic_fetch_add(&ws_done(P)[o], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(256) init_kernel(Params P) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    *ws_remaining(P) = static_cast<uint32_t>(P.batch);
+    *ws_abort(P) = 0u;
+    *ws_next_tree(P) = 0u;
+  }
+  if (i < P.grid) {
+    ws_words(P)[i] = 0ull;
+    ws_done(P)[i] = 0u;
+  }
+  if (i < P.batch) {
+    P.status[i] = TV_TREE_ABORTED;
+    P.accept_len[i] = -1;
+    P.accepted_node[i] = -1;
+    P.bonus_token[i] = -1;
+  }
+}
+
+template <typename T, class A, int kCap>
+__global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
+  __shared__ TreeSmem<kCap> sm_;
+  __shared__ WgScratch ws_;
+  __shared__ Params Ps_;     // for the controller, which is not inlined
+  Lds<TreeSmem<kCap>>& sm = lds_ref(sm_);
+  Lds<WgScratch>& ws = lds_ref(ws_);
+  Lds<Params>& Ps = lds_ref(Ps_);
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    Ps_ = P;
+    sm.has_tree = 0;
+    sm.pending = 0;
+    sm.seq = 0;
+    sm.expect_done = 0;
+    ws.trees_left = 1;
+    ws.scan_pos = static_cast<int>(blockIdx.x);
+  }
+  __syncthreads();
+  for (;;) {
+    if (tid < 64) {
+      const int ev = wait_event(sm, ws, P);
+      if (tid == 0) ws.event = ev;
+    }
+    __syncthreads();
+    const int ev = ws.event;
+    if (ev == kEvExit) break;
+    // The owner's work (its own items, its controller) is on its tree's
+    // critical path: it gets issue priority over other waves of the CU.
+    if (sm.has_tree || ev != kEvItem) __builtin_amdgcn_s_setprio(2);
+    if (ev == kEvItem) {
+      run_segment<T, A>(ws, P, ar);
+    } else {
+      if (ev == kEvTree) begin_tree<T>(sm, Ps, ws.new_tree);
+      owner_step<T, A>(sm, ws, Ps, ar);
+    }
+    __builtin_amdgcn_s_setprio(0);
   }
 }
 
@@ -1129,26 +1797,47 @@ __global__ void __launch_bounds__(kThreads) verify_kernel(Params P, A ar) {
 // with few elements the per-element rounding of the fast path does not average.
 constexpr int kPreciseBelowVocab = 16384;
 
-template <typename T, int algo>
-int launch_typed(const Params& P, bool precise, int batch, hipStream_t stream) {
-  const dim3 grid(static_cast<unsigned>(batch));
-  const dim3 block(kThreads);
-  if (precise) {
-    PreciseArith ar{P.k64};
-    hipLaunchKernelGGL((verify_kernel<T, PreciseArith, algo>), grid, block, 0, stream, P, ar);
-  } else {
-    FastArith ar{P.k32};
-    hipLaunchKernelGGL((verify_kernel<T, FastArith, algo>), grid, block, 0, stream, P, ar);
-  }
+template <typename T, class A, int kCap>
+int launch_typed(Params P, const A& ar, int slots, hipStream_t stream) {
+  int dev = 0, cus = 0, clock_khz = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return TV_ERR_HIP;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+    return TV_ERR_HIP;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, verify_kernel<T, A, kCap>, kNT, 0) !=
+      hipSuccess)
+    return TV_ERR_HIP;
+  if (per_cu < 1) per_cu = 1;
+  // every workgroup spins until the launch is over, so the grid is at most
+  // what can be resident at once; more than one per segment in flight is useless
+  long long grid = static_cast<long long>(per_cu) * (cus > 0 ? cus : 1);
+  if (grid > slots) grid = slots;
+  if (grid < 1) grid = 1;
+  P.grid = static_cast<int>(grid);
+  P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s without progress
+  const int init_n = P.batch > P.grid ? P.batch : P.grid;
+  hipLaunchKernelGGL(init_kernel, dim3((init_n + 255) / 256), dim3(256), 0, stream, P);
+  if (hipGetLastError() != hipSuccess) return TV_ERR_HIP;
+  hipLaunchKernelGGL((verify_kernel<T, A, kCap>), dim3(static_cast<unsigned>(grid)), dim3(kNT),
+                     0, stream, P, ar);
   return hipGetLastError() == hipSuccess ? TV_OK : TV_ERR_HIP;
+}
+
+template <typename T, int kCap>
+int launch_cap(const Params& P, bool precise, int slots, hipStream_t stream) {
+  if constexpr (sizeof(T) == 2) {
+    if (!precise) return launch_typed<T, FastArith, kCap>(P, FastArith{P.k32}, slots, stream);
+  }
+  return launch_typed<T, PreciseArith, kCap>(P, PreciseArith{P.k64}, slots, stream);
 }
 
 }  // namespace
 
 namespace tv {
 
-int launch(const VerifyArgs& a, Algo algo, hipStream_t stream) {
-  Params P;
+int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) {
+  const WorkspaceLayout L = workspace_layout(a.batch, a.vocab);
+  Params P{};
   P.parents = a.parents;
   P.tokens = a.tokens;
   P.target = a.target;
@@ -1162,19 +1851,26 @@ int launch(const VerifyArgs& a, Algo algo, hipStream_t stream) {
   P.node_theta = a.node_theta;
   P.p_init = a.p_init;
   P.counters = a.counters;
+  P.ws = static_cast<uint8_t*>(workspace);
+  P.off_words = L.off_words;
+  P.off_done = L.off_done;
+  P.off_desc = L.off_desc;
+  P.off_parts = L.off_parts;
+  P.seg_stride = L.seg_stride;
+  P.batch = a.batch;
   P.num_nodes = a.num_nodes;
   P.vocab = a.vocab;
   P.mode = a.mode;
+  P.algo = static_cast<int>(algo);
   P.k64 = 1.4426950408889634 / static_cast<double>(a.temperature);
   P.k32 = static_cast<float>(P.k64);
   const bool precise = a.dtype == TV_DTYPE_F32 || a.vocab < kPreciseBelowVocab;
-  constexpr int kTv = static_cast<int>(Algo::kTraversal);
-  constexpr int kTl = static_cast<int>(Algo::kTokenLevel);
+  const bool small = a.num_nodes <= kCapSmall;
   if (a.dtype == TV_DTYPE_BF16)
-    return algo == Algo::kTraversal ? launch_typed<uint16_t, kTv>(P, precise, a.batch, stream)
-                                    : launch_typed<uint16_t, kTl>(P, precise, a.batch, stream);
-  return algo == Algo::kTraversal ? launch_typed<float, kTv>(P, precise, a.batch, stream)
-                                  : launch_typed<float, kTl>(P, precise, a.batch, stream);
+    return small ? launch_cap<uint16_t, kCapSmall>(P, precise, L.slots, stream)
+                 : launch_cap<uint16_t, kCapLarge>(P, precise, L.slots, stream);
+  return small ? launch_cap<float, kCapSmall>(P, true, L.slots, stream)
+               : launch_cap<float, kCapLarge>(P, true, L.slots, stream);
 }
 
 }  // namespace tv

@@ -41,6 +41,7 @@ def test_constants_match_header():
         line = re.search(rf"#define {name}\s+([^\n]+)", text).group(1)
         return line.split("/*")[0].strip()
 
+    assert eval(define("TV_MAX_BATCH")) == tv.TV_MAX_BATCH
     assert eval(define("TV_MAX_NODES")) == tv.TV_MAX_NODES
     assert eval(define("TV_MAX_VOCAB")) == tv.TV_MAX_VOCAB
     assert eval(define("TV_MAX_VOCAB_F32")) == tv.TV_MAX_VOCAB_F32
@@ -49,7 +50,7 @@ def test_constants_match_header():
                  "TV_ERR_HIP", "TV_DTYPE_BF16", "TV_DTYPE_F32", "TV_SIBLINGS_WITHOUT_REPLACEMENT",
                  "TV_SIBLINGS_WITH_REPLACEMENT", "TV_TREE_OK", "TV_TREE_BAD_PARENT",
                  "TV_TREE_BAD_TOKEN", "TV_TREE_DUP_SIBLING", "TV_TREE_NONFINITE",
-                 "TV_TREE_DEGENERATE", "TV_NODE_UNTESTED", "TV_NODE_ACCEPTED",
+                 "TV_TREE_DEGENERATE", "TV_TREE_ABORTED", "TV_NODE_UNTESTED", "TV_NODE_ACCEPTED",
                  "TV_NODE_REJECTED", "TV_NODE_PRUNED"]:
         m = re.search(rf"\b{name}\s*=\s*(\d+)", text)
         assert m and int(m.group(1)) == getattr(tv, name), name
@@ -62,18 +63,33 @@ def test_status_strings():
     assert tv.tv_status_string(99) == "unknown status"
 
 
-def test_workspace_size_is_zero():
-    assert tv.tv_workspace_size(256, 65, 128256) == 0
+def test_workspace_size():
+    ws = tv.tv_workspace_size
+    # invalid sizes report 0
+    for args in [(0, 65, 1000), (-1, 65, 1000), (1, 0, 1000), (1, tv.TV_MAX_NODES + 1, 1000),
+                 (1, 65, 1), (1, 65, tv.TV_MAX_VOCAB + 1), (tv.TV_MAX_BATCH + 1, 65, 1000)]:
+        assert ws(*args) == 0, args
+    # positive, 256-byte granular, monotone in batch and vocabulary, bounded
+    sizes = [ws(b, 65, 128256) for b in (1, 2, 16, 256, 4096, tv.TV_MAX_BATCH)]
+    assert all(s > 0 and s % 256 == 0 for s in sizes)
+    assert sizes == sorted(sizes)
+    assert sizes[-1] == sizes[-2]          # capped by the number of workgroups per call
+    assert ws(16, 65, 2) <= ws(16, 65, 128256) <= ws(16, 65, tv.TV_MAX_VOCAB)
+    assert ws(tv.TV_MAX_BATCH, tv.TV_MAX_NODES, tv.TV_MAX_VOCAB) <= 65 << 20
+    # independent of the tree size
+    assert ws(256, 2, 128256) == ws(256, tv.TV_MAX_NODES, 128256)
 
 
 # Fake, never-dereferenced device addresses: validation fails before any HIP call.
 A = 0x10000
+WS = 0x40000000
 
 
 def call(fn="tv_verify", **kw):
     args = dict(batch=2, num_nodes=5, vocab=100, parents=A, tokens=A, target_logits=A,
                 draft_logits=A + 0x1000, dtype=tv.TV_DTYPE_BF16, temperature=1.0, uniforms=A,
-                mode=0, accept_len=A, accepted_node=A, bonus_token=A, status=A)
+                mode=0, accept_len=A, accepted_node=A, bonus_token=A, status=A,
+                workspace=WS, workspace_bytes=tv.tv_workspace_size(2, 5, 100))
     args.update(kw)
     return getattr(tv, fn)(**args)
 
@@ -109,6 +125,10 @@ def call(fn="tv_verify", **kw):
     (dict(target_logits=A + 2, draft_logits=A + 4), tv.TV_ERR_UNSUPPORTED),
     (dict(parents=A + 2), tv.TV_ERR_INVALID_ARG),
     (dict(counters=A + 1), tv.TV_ERR_INVALID_ARG),
+    (dict(batch=tv.TV_MAX_BATCH + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(workspace=None), tv.TV_ERR_WORKSPACE),
+    (dict(workspace=WS + 128), tv.TV_ERR_WORKSPACE),
+    (dict(workspace_bytes=256), tv.TV_ERR_WORKSPACE),
 ])
 def test_host_validation(fn, kw, want):
     assert call(fn, **kw) == want
