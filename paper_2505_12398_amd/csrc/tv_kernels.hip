@@ -1,21 +1,17 @@
 // Traversal Verification (arXiv 2505.12398, Algorithm 3) and the token-level
 // baseline (Sec. 2.2, Algorithm 2 per node) for gfx950 (MI355X, CDNA4).
 //
-// Work split. A workgroup that has no tree claims the next one from a
-// launch-wide counter and becomes its owner: it holds the tree in LDS and
-// runs the sequential traversal on thread 0. Whenever the traversal needs a
-// vocabulary-wide quantity it publishes a batch of passes, each cut into
-// segments of 2048 16-byte vectors of a node's rows; workgroups without a tree
-// claim segments of any published batch (an owner works on its own), compute
-// the segment's partial result and report it. When all segments of its batch
-// are in, the owner combines the partials in segment order and continues. So a
-// tree whose traversal needs many passes is served by many CUs, and the
-// per-tree load imbalance of the method does not leave CUs idle.
-//
-// A batch holds the pass the traversal needs now plus the STATS passes of the
-// nodes it will descend into next (the internal nodes on the leftmost
-// remaining path below the next child); those depend only on their own rows,
-// so they run alongside instead of one after another.
+// Work split. Each tree is verified by a group of G workgroups (G chosen per
+// launch so that the groups fill the device: G is large for small batches and
+// small for large ones). Every member of a group holds the tree in LDS and runs
+// the same sequential traversal on its thread 0, on the same data, so all
+// members take the same decisions. Whenever the traversal needs vocabulary-wide
+// quantities, each member computes its fixed 1/G stripe of the rows involved,
+// publishes the stripe's partial results and waits for the other members';
+// every member then combines the G partials in member order and continues.
+// The group only exchanges these partials: one atomic counter per group and a
+// few words per member and pass. The launch is cooperative, so all members of
+// a group are resident together.
 //
 // Pass kinds:
 //   STATS   per row: maximum and sum of 2^(z*k - max*k), k = log2(e)/T, over
@@ -26,9 +22,13 @@
 //           rejection: Eq. (e1) and (e3);
 //   WSUM    the same weights as SPASS without updating anything (only needed
 //           when Y is drawn at a node whose last pass was not its SPASS).
-// Y is drawn by inverse CDF in ascending token order: the segment partials of
-// the pass that produced the weights locate the segment holding u*W, and the
-// owner rescans that one segment.
+// Passes are issued in batches: the pass the traversal needs now plus the
+// STATS passes of the internal nodes it will descend into next (the nodes on
+// the leftmost remaining path below the next child); those depend only on
+// their own rows, so they are computed with it instead of one after another.
+// Y is drawn by inverse CDF in ascending token order: the stripe partials of
+// the pass that produced the weights locate the stripe holding u*W, and one
+// member rescans that stripe.
 //
 // A node's residual target and draft are never materialised: after k
 // rejections they are b = [A p - B q]_+ and s = c q off the rejected tokens,
@@ -41,21 +41,18 @@
 // V < 16384) evaluates every term in fp64. The remaining draft mass after Eq.
 // (e2) is the pass's own sum of draft terms minus the rejected tokens' terms,
 // never 1 - sum q(rejected), which cancels when those held most of the mass.
-// Every sum is formed in a fixed order (per thread, then across the
-// workgroup, then across segments), so results do not depend on which
-// workgroup processed which segment.
+// Every sum is formed in a fixed order (per thread, across the workgroup, then
+// across members), so results are reproducible for a given group size.
 //
-// Synchronisation. Data shared between workgroups (segment results, pass
-// parameters) is written with agent-scope atomic stores, which write through
-// to the device-coherent level, and the writer waits for those stores to be
-// acknowledged before it signals (atomic increment of the owner's counter, or
-// atomic store of its work word). This orders data before signal the way an
-// agent-scope release fence would, without the fence's write-back of the
-// whole L2. Readers observe the signal with an atomic load, issue an
-// agent-scope acquire fence and read the data with agent-scope atomic loads.
-// Every wait is bounded by a wall-clock limit after which the launch is
-// abandoned (trees not finished then report TV_TREE_ABORTED), so no wave can
-// spin forever.
+// Synchronisation. A member writes its partials with agent-scope atomic stores
+// (written through to the device-coherent level), waits for them to be
+// acknowledged, then increments the group's counter; members wait until the
+// counter reaches G times the batch number, issue an agent-scope acquire fence
+// and read the partials with agent-scope atomic loads. Partials are double
+// buffered by batch parity: a member can only start batch k+2 after every
+// member has finished batch k+1, hence has read batch k. Every wait is bounded
+// by a wall-clock limit after which the launch is abandoned (trees not
+// finished then report TV_TREE_ABORTED), so no wave can spin forever.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -69,61 +66,24 @@ namespace {
 
 constexpr int kNT = 256;                       // threads per workgroup
 constexpr int kNW = kNT / 64;
-constexpr int kSegVec = tv::kSegVec;
-constexpr int kVecPerThread = kSegVec / kNT;   // vectors per row per thread and segment
 // vectors per row in flight per lane: the fp64 element path needs more registers
 template <class A> constexpr int kUnrollOf = A::kPrecise ? 2 : 4;
 constexpr int kCapSmall = 128;                 // node capacity of the compact variant
 constexpr int kCapLarge = TV_MAX_NODES;
-static_assert(kSegVec % (kNT * 4) == 0, "segment must be whole rounds");
-static_assert(tv::kMaxSeg <= 64, "segments are combined by one wavefront");
+constexpr int kMaxBatch = tv::kMaxBatchPasses; // passes per batch
+constexpr int kMaxGroup = tv::kMaxGroup;       // workgroups per tree
+static_assert(kMaxGroup <= 64, "member partials are combined by one wavefront");
 
-// Pass kinds (4 bits each in a batch descriptor) and owner-internal commands.
+// Pass kinds and controller commands.
 enum : int {
   kCmdNone = 0, kCmdStats2 = 1, kCmdStats1 = 2, kCmdSPass = 3, kCmdSPassSd = 4, kCmdWSum = 5,
-  kCmdLocalSample = 6, kCmdDone = 7
+  kCmdLocalSample = 6, kCmdDone = 7, kCmdBatch = 8
 };
-enum : int { kEvItem = 0, kEvOwn = 1, kEvTree = 2, kEvExit = 3 };
 enum : int {
   kPhDescend = 0, kPhTest, kPhAfterSPass, kPhFinal, kPhFinalLeafStats, kPhFinalWSum,
   kPhAfterSample, kPhPinit, kPhTlVisit, kPhTlAfterSPass
 };
 enum : uint8_t { kFlagStats = 1, kFlagConsulted = 2, kFlagBad = 4, kFlagSd = 8 };
-
-constexpr int kMaxBatch = tv::kMaxBatchPasses;   // passes per batch
-
-// Work word of an owner slot: the batch it offers and how many items are taken.
-// Item i of a batch is segment i % nseg of pass i / nseg.
-//   bits  0-12 items claimed so far (may run past the total: extra claims are void)
-//   bits 13-22 items of the batch (0: nothing offered)
-//   bits 23-29 segments per pass
-//   bits 30-49 tree (batch index)
-//   bits 50-63 sequence number of the batch (low 14 bits), repeated in the descriptor
-struct Work {
-  int cnt, total, nseg, tree, seq;
-};
-__device__ __forceinline__ uint64_t pack_work(int total, int nseg, int tree, int seq) {
-  return (static_cast<uint64_t>(total) << 13) | (static_cast<uint64_t>(nseg) << 23) |
-         (static_cast<uint64_t>(tree) << 30) | (static_cast<uint64_t>(seq & 0x3FFF) << 50);
-}
-__device__ __forceinline__ Work unpack_work(uint64_t w) {
-  return Work{static_cast<int>(w & 0x1FFFu), static_cast<int>((w >> 13) & 0x3FFu),
-              static_cast<int>((w >> 23) & 0x7Fu), static_cast<int>((w >> 30) & 0xFFFFFu),
-              static_cast<int>((w >> 50) & 0x3FFFu)};
-}
-
-// Batch descriptor (8 words per owner slot):
-//   [0..3] multipliers and frames (ap, bp, cb, cs) of the batch's SPASS / WSUM pass
-//   [4], [5] nodes of passes 0-3 and 4-7 (16 bits each)
-//   [6] pass kinds (4 bits each)
-//   [7] sequence number of the batch
-constexpr int kDescWords = 8;
-__device__ __forceinline__ int desc_node(const uint64_t (&d)[kDescWords], int p) {
-  return static_cast<int>((d[4 + (p >> 2)] >> (16 * (p & 3))) & 0xFFFFu);
-}
-__device__ __forceinline__ int desc_cmd(const uint64_t (&d)[kDescWords], int p) {
-  return static_cast<int>((d[6] >> (4 * p)) & 0xFu);
-}
 
 struct Params {
   const int32_t* parents;
@@ -140,15 +100,15 @@ struct Params {
   float* p_init;
   int32_t* counters;
   uint8_t* ws;
-  size_t off_words, off_done, off_desc, off_parts;
-  long long spin_limit;      // wall-clock ticks without progress before the launch is abandoned
+  size_t off_counters, off_parts;
+  long long spin_limit;      // wall-clock ticks a wait may last before the launch is abandoned
   int batch;
   int num_nodes;
   int vocab;
   int mode;
   int algo;
-  int grid;                  // workgroups, one workspace slot each
-  int seg_stride;            // partial-result slots per workgroup
+  int G;                     // workgroups per group (per tree)
+  int ngroups;               // groups; group g verifies trees g, g + ngroups, ...
   float k32;                 // log2(e) / T rounded to fp32 (fast element path)
   double k64;                // log2(e) / T (precise element path)
 };
@@ -162,7 +122,7 @@ __device__ __forceinline__ Lds<X>& lds_ref(X& x) {
   return *reinterpret_cast<Lds<X>*>((__attribute__((address_space(3))) void*)&x);
 }
 
-struct SegPart {             // 32 bytes
+struct SegPart {             // 32 bytes: one member's partial result of one pass
   double s0, s1;
   float m0, m1;
   uint32_t pad[2];
@@ -173,33 +133,19 @@ struct SegPart {             // 32 bytes
 // ---------------------------------------------------------------------------
 
 template <class PP>
-__device__ __forceinline__ uint32_t* ws_remaining(const PP& P) {
+__device__ __forceinline__ uint32_t* ws_abort(const PP& P) {
   return reinterpret_cast<uint32_t*>(P.ws);
 }
 template <class PP>
-__device__ __forceinline__ uint32_t* ws_abort(const PP& P) {
-  return reinterpret_cast<uint32_t*>(P.ws + 256);
+__device__ __forceinline__ uint32_t* ws_counter(const PP& P, int g) {
+  return reinterpret_cast<uint32_t*>(P.ws + P.off_counters + static_cast<size_t>(g) *
+                                                                 tv::kCounterStride);
 }
+// partial of member m for pass p of the batch with parity `par` in group g
 template <class PP>
-__device__ __forceinline__ uint32_t* ws_next_tree(const PP& P) {
-  return reinterpret_cast<uint32_t*>(P.ws + 512);
-}
-template <class PP>
-__device__ __forceinline__ uint64_t* ws_words(const PP& P) {
-  return reinterpret_cast<uint64_t*>(P.ws + P.off_words);
-}
-template <class PP>
-__device__ __forceinline__ uint32_t* ws_done(const PP& P) {
-  return reinterpret_cast<uint32_t*>(P.ws + P.off_done);
-}
-template <class PP>
-__device__ __forceinline__ uint64_t* ws_desc(const PP& P, int o) {
-  return reinterpret_cast<uint64_t*>(P.ws + P.off_desc) + kDescWords * static_cast<size_t>(o);
-}
-template <class PP>
-__device__ __forceinline__ SegPart* ws_parts(const PP& P, int o, int pass) {
+__device__ __forceinline__ SegPart* ws_parts(const PP& P, int g, int par, int p) {
   return reinterpret_cast<SegPart*>(P.ws + P.off_parts) +
-         (static_cast<size_t>(o) * kMaxBatch + pass) * P.seg_stride;
+         ((static_cast<size_t>(g) * 2 + par) * kMaxBatch + p) * P.G;
 }
 
 __device__ __forceinline__ uint64_t ld_rlx(const uint64_t* p) {
@@ -229,12 +175,6 @@ __device__ __forceinline__ void fence_acquire() { __builtin_amdgcn_fence(__ATOMI
 __device__ __forceinline__ void stores_done() {
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
-__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
-  const uint32_t lo = __shfl(static_cast<uint32_t>(v), src, 64);
-  const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, 64);
-  return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 // ---------------------------------------------------------------------------
@@ -282,9 +222,20 @@ __device__ __forceinline__ Geom row_geom(const T* row, int V) {
   return Geom{head, rest / E, rest % E};
 }
 
-__device__ __forceinline__ int num_segments(const Geom& g) {
-  const int s = (g.nvec + kSegVec - 1) / kSegVec;
-  return s < 1 ? 1 : s;
+// The stripe of member m of G: vectors [vb, ve); member 0 also holds the head
+// elements and member G-1 the tail elements.
+struct SegRange {
+  int vb, ve;
+  bool first, last;
+};
+
+__device__ __forceinline__ SegRange stripe(const Geom& g, int m, int G) {
+  SegRange r;
+  r.vb = static_cast<int>((static_cast<long long>(g.nvec) * m) / G);
+  r.ve = static_cast<int>((static_cast<long long>(g.nvec) * (m + 1)) / G);
+  r.first = m == 0;
+  r.last = m == G - 1;
+  return r;
 }
 
 template <typename T>
@@ -308,17 +259,11 @@ struct WgScratch {
   double red_d[2 * kNW];
   float red_f[2 * kNW];
   double scan_d[kNW];
-  int event;
-  int item_owner;
-  uint64_t item_word;
-  uint64_t item_desc[kDescWords];
-  int scan_pos;
-  int new_tree;             // tree just claimed (kEvTree)
-  int trees_left;           // 0 once the tree counter ran past the batch
+  int stop;                 // the launch was abandoned
   int hit;                  // first thread whose range holds the sample
   int last_pos;             // last thread with positive weight
   int smp_seg;
-  double smp_target;        // mass still to cover inside the chosen segment
+  double smp_target;        // mass still to cover inside the chosen stripe
 };
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -567,28 +512,15 @@ __device__ __forceinline__ double scalar_weight(const TM& tm, const T* rb, const
 }
 
 // ---------------------------------------------------------------------------
-// Segment passes (any workgroup). Thread t takes vectors vb + t + i * kNT of
-// the segment; segment 0 also holds the head elements and the last segment
-// the tail elements. Per thread: head, vectors in order, tail.
+// Stripe passes. Thread t takes vectors vb + t + i * kNT of the stripe; per
+// thread: head elements, vectors in order, tail elements. Loads are
+// unconditional (indices clamped into the stripe) so that all of a round's
+// loads are in flight together; only the arithmetic is guarded.
 // ---------------------------------------------------------------------------
 
-struct SegRange {
-  int vb, ve;          // vectors [vb, ve)
-  bool first, last;
-};
-
-__device__ __forceinline__ SegRange seg_range(const Geom& g, int seg, int nseg) {
-  SegRange r;
-  r.vb = seg * kSegVec;
-  r.ve = min(g.nvec, r.vb + kSegVec);
-  r.first = seg == 0;
-  r.last = seg == nseg - 1;
-  return r;
-}
-
 template <typename T, class A, bool TWO>
-__device__ void seg_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
-                          const SegRange& r, const A& ar, SegPart& out) {
+__device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
+                             const SegRange& r, const A& ar, SegPart& out) {
   constexpr int E = Elem<T>::E;
   constexpr int kUnroll = kUnrollOf<A>;
   const int tid = threadIdx.x;
@@ -601,14 +533,12 @@ __device__ void seg_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Ge
       online_add(os, xs, ar);
     }
   }
-  // Loads are unconditional (indices clamped into the segment) so that all of
-  // a round's loads are in flight together; only the arithmetic is guarded.
 #pragma unroll 1
-  for (int i0 = 0; i0 < kVecPerThread && i0 * kNT < r.ve - r.vb; i0 += kUnroll) {
+  for (int base = r.vb; base < r.ve; base += kNT * kUnroll) {
     uint4 lb[kUnroll], ls[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int v = min(r.vb + tid + (i0 + u) * kNT, r.ve - 1);
+      const int v = min(base + tid + u * kNT, r.ve - 1);
       lb[u] = load16(rb, g.head, v);
       if constexpr (TWO) ls[u] = load16(rs, g.head, v);
     }
@@ -619,8 +549,7 @@ __device__ void seg_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Ge
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int v = r.vb + tid + (i0 + u) * kNT;
-      if (v < r.ve) {
+      if (base + tid + u * kNT < r.ve) {
         float x[E];
         Elem<T>::unpack(lb[u], x);
         online_add(ob, x, ar);
@@ -643,7 +572,7 @@ __device__ void seg_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Ge
   float Mb = ob.m, Ms = TWO ? os.m : -INFINITY;
   block_max2(ws, Mb, Ms);
   // exact fp64 change of frame; a thread that saw no finite value has s = 0
-  // (or NaN) and the factor 0. A segment with no finite value keeps s = 0 (or
+  // (or NaN) and the factor 0. A stripe with no finite value keeps s = 0 (or
   // NaN) and maximum -inf.
   double Sb = (Mb > -INFINITY) ? ob.s * exp2(ar.frame(Mb) - ob.c) : ob.s;
   double Ss = (TWO && Ms > -INFINITY) ? os.s * exp2(ar.frame(Ms) - os.c) : (TWO ? os.s : 0.0);
@@ -655,20 +584,20 @@ __device__ void seg_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Ge
 }
 
 template <typename T, class A, bool SD>
-__device__ void seg_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
-                         const SegRange& r, const A& ar, const TermParams& p, SegPart& out) {
+__device__ void stripe_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
+                            const SegRange& r, const A& ar, const TermParams& p, SegPart& out) {
+  constexpr int kUnroll = kUnrollOf<A>;
   const Terms<A, true, SD> tm(ar, p);
   using TM = Terms<A, true, SD>;
-  constexpr int kUnroll = kUnrollOf<A>;
   const int tid = threadIdx.x;
   double acc = 0.0, sd = 0.0;
   if (r.first && tid < g.head) acc += scalar_weight<T, TM, true>(tm, rb, rs, tid, sd);
 #pragma unroll 1
-  for (int i0 = 0; i0 < kVecPerThread && i0 * kNT < r.ve - r.vb; i0 += kUnroll) {
+  for (int base = r.vb; base < r.ve; base += kNT * kUnroll) {
     uint4 lb[kUnroll], ls[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int v = min(r.vb + tid + (i0 + u) * kNT, r.ve - 1);
+      const int v = min(base + tid + u * kNT, r.ve - 1);
       lb[u] = load16(rb, g.head, v);
       ls[u] = load16(rs, g.head, v);
     }
@@ -678,10 +607,8 @@ __device__ void seg_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geo
       pin(ls[u]);
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int v = r.vb + tid + (i0 + u) * kNT;
-      if (v < r.ve) acc += vec_sum<T, TM, true>(tm, lb[u], ls[u], sd);
-    }
+    for (int u = 0; u < kUnroll; ++u)
+      if (base + tid + u * kNT < r.ve) acc += vec_sum<T, TM, true>(tm, lb[u], ls[u], sd);
   }
   if (r.last && tid < g.tail)
     acc += scalar_weight<T, TM, true>(tm, rb, rs, g.head + g.nvec * Elem<T>::E + tid, sd);
@@ -693,10 +620,8 @@ __device__ void seg_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geo
 }
 
 // ---------------------------------------------------------------------------
-// Owner state (LDS) and the scalar traversal logic (thread 0)
+// Tree state (LDS) and the scalar traversal logic (thread 0)
 // ---------------------------------------------------------------------------
-
-enum : int { kCmdBatch = 8 };      // controller command: publish the batch in sm.b*
 
 template <int kCap>
 struct TreeSmem {
@@ -740,10 +665,8 @@ struct TreeSmem {
   int8_t bcmd[kMaxBatch];
   double cmd_ap, cmd_bp, cmd_cb, cmd_cs;    // parameters of a SPASS / WSUM pass 0
   // the batch in flight, then just completed
-  int pending, bnseg;
-  uint32_t seq;                    // batches published by this workgroup
-  uint32_t expect_done;            // value of this slot's done counter that completes the batch
-  uint64_t desc[kDescWords];       // the published descriptor (the owner claims from it)
+  int pending;
+  uint32_t seq;                    // batches this group has run (all trees so far)
   int spass_node;                  // node whose SPASS partials are in the workspace (-1: none)
   double last_ap, last_bp, last_cb, last_cs;
   // local sample request
@@ -1111,7 +1034,7 @@ __device__ __attribute__((always_inline)) void advance(Lds<TreeSmem<kCap>>& sm, 
 }
 
 // ---------------------------------------------------------------------------
-// Owner: tree set-up, combining a completed batch, local sample, publishing
+// Tree set-up and outputs
 // ---------------------------------------------------------------------------
 
 template <typename T, class PP>
@@ -1216,7 +1139,7 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, co
   __syncthreads();
 }
 
-// Writes the tree's outputs (all threads) and retires it.
+// Writes the tree's outputs (all threads of one member).
 template <int kCap>
 __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& sm,
                                                            const Lds<Params>& P) {
@@ -1242,73 +1165,33 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
       c[2] = ok ? (sm.child_count[sm.accepted] == 0 ? 1 : 0) : 0;
       c[3] = ok ? sm.tests : 0;
     }
-    // withdraw the offer (nothing left to claim) and retire the tree
-    st_rlx(&ws_words(P)[blockIdx.x], 0ull);
-    __hip_atomic_fetch_sub(ws_remaining(P), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     sm.has_tree = 0;
   }
   __syncthreads();
 }
 
-// Publishes the batch the controller asked for (thread 0).
-template <typename T, int kCap>
-__device__ __attribute__((always_inline)) void publish(Lds<TreeSmem<kCap>>& sm,
-                                                       const Lds<Params>& P) {
-  if (threadIdx.x == 0) {
-    const int b = sm.tree;
-    const int bn = sm.bn;
-    int nseg = 1;
-    uint64_t nodes[2] = {0, 0}, cmds = 0;
-    for (int p = 0; p < bn; ++p) {
-      const int node = sm.bnode[p];
-      nseg = max(nseg, num_segments(row_geom(row_ptr<T>(P, P.target, b, node), P.vocab)));
-      nodes[p >> 2] |= static_cast<uint64_t>(node) << (16 * (p & 3));
-      cmds |= static_cast<uint64_t>(sm.bcmd[p]) << (4 * p);
-    }
-    const uint32_t seq = ++sm.seq;
-    uint64_t d[kDescWords] = {
-        static_cast<uint64_t>(__double_as_longlong(sm.cmd_ap)),
-        static_cast<uint64_t>(__double_as_longlong(sm.cmd_bp)),
-        static_cast<uint64_t>(__double_as_longlong(sm.cmd_cb)),
-        static_cast<uint64_t>(__double_as_longlong(sm.cmd_cs)),
-        nodes[0], nodes[1], cmds, seq};
-    uint64_t* g = ws_desc(P, blockIdx.x);
-    for (int i = 0; i < kDescWords; ++i) {
-      sm.desc[i] = d[i];
-      st_rlx(g + i, d[i]);
-    }
-    const int cmd0 = sm.bcmd[0];
-    sm.pending = 1;
-    sm.bnseg = nseg;
-    sm.last_ap = sm.cmd_ap;
-    sm.last_bp = sm.cmd_bp;
-    sm.last_cb = sm.cmd_cb;
-    sm.last_cs = sm.cmd_cs;
-    sm.spass_node = (cmd0 == kCmdSPass || cmd0 == kCmdSPassSd) ? sm.bnode[0] : -1;
-    sm.expect_done += static_cast<uint32_t>(bn * nseg);
-    stores_done();
-    st_rlx(&ws_words(P)[blockIdx.x], pack_work(bn * nseg, nseg, b, static_cast<int>(seq)));
-  }
-  __syncthreads();
-}
+// ---------------------------------------------------------------------------
+// Group exchange: combining the members' partials, the local sample
+// ---------------------------------------------------------------------------
 
-// Combines the segment partials of the completed batch (all threads): wave w
-// takes passes w, w + 4; STATS results go to the node arrays, a SPASS / WSUM
-// result to res_S / res_sd.
+// Combines the members' partials of the completed batch (all threads): wave w
+// takes passes w, w + 4, lanes are members; STATS results go to the node
+// arrays, a SPASS / WSUM result to res_S / res_sd.
 template <typename T, class A, int kCap>
 __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
-                                                       const Lds<Params>& P, A ar) {
+                                                       const Lds<Params>& P, A ar, int g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bn = sm.bn;
-  const int nseg = sm.bnseg;
+  const int G = P.G;
+  const int par = static_cast<int>(sm.seq & 1u);
   fence_acquire();
   for (int p = wave; p < bn; p += kNW) {
     const int cmd = sm.bcmd[p];
     const int node = sm.bnode[p];
-    const SegPart* part = ws_parts(P, blockIdx.x, p);
+    const SegPart* part = ws_parts(P, g, par, p);
     double s0 = 0.0, s1 = 0.0;
     float m0 = -INFINITY, m1 = -INFINITY;
-    if (lane < nseg) {
+    if (lane < G) {
       s0 = ld_rlx_f64(&part[lane].s0);
       s1 = ld_rlx_f64(&part[lane].s1);
       const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
@@ -1321,7 +1204,7 @@ __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
       const float Ms = two ? wave_max(m1) : -INFINITY;
       const double Cb = ar.frame(Mb);
       const double Cs = two ? ar.frame(Ms) : 0.0;
-      // segment sums in the row's frame; a segment with no finite value adds 0 (or NaN)
+      // stripe sums in the row's frame; a stripe with no finite value adds 0 (or NaN)
       double tb = (m0 > -INFINITY) ? s0 * exp2(Cb - ar.frame(m0)) : s0;
       double ts = two ? ((m1 > -INFINITY) ? s1 * exp2(Cs - ar.frame(m1)) : s1) : 0.0;
       tb = __shfl(wave_sum(tb), 0, 64);
@@ -1366,20 +1249,20 @@ __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
   __syncthreads();
 }
 
-// Inverse-CDF draw of Y (all threads). The weights of the segments come from the
-// partials of pass 0 of the batch just completed; the segment holding u*W is
-// rescanned.
+// Inverse-CDF draw of Y (all threads of one member). The weights of the
+// stripes come from the partials of pass 0 of the batch just completed; the
+// stripe holding u*W is rescanned.
 template <typename T, class A, int kCap>
 __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
-                                                       const Lds<Params>& P, A ar) {
+                                                       const Lds<Params>& P, A ar, int g) {
   constexpr int E = Elem<T>::E;
   const int tid = threadIdx.x, lane = tid & 63;
   const int node = sm.bnode[0];
-  const int nseg = sm.bnseg;
+  const int G = P.G;
   if (tid < 64) {
-    const SegPart* part = ws_parts(P, blockIdx.x, 0);
+    const SegPart* part = ws_parts(P, g, static_cast<int>(sm.seq & 1u), 0);
     double w = 0.0;
-    if (lane < nseg) {
+    if (lane < G) {
       const double s0 = ld_rlx_f64(&part[lane].s0);
       if (sm.smp_from_stats) {
         const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
@@ -1395,16 +1278,16 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
       const double o = __shfl_up(incl, off, 64);
       if (lane >= off) incl += o;
     }
-    const double W = __shfl(incl, nseg - 1, 64);
+    const double W = __shfl(incl, G - 1, 64);
     const double target = static_cast<double>(sm.u[0]) * W;
-    const uint64_t pos = __ballot(lane < nseg && w > 0.0);
-    const uint64_t hits = __ballot(lane < nseg && w > 0.0 && target < incl);
+    const uint64_t pos = __ballot(lane < G && w > 0.0);
+    const uint64_t hits = __ballot(lane < G && w > 0.0 && target < incl);
     int seg = -1;
     bool fallback = false;
     if (W > 0.0 && isfinite(W) && pos != 0) {
       if (hits) {
         seg = __ffsll(static_cast<long long>(hits)) - 1;
-      } else {                              // rounding at the end: last segment with mass
+      } else {                              // rounding at the end: last stripe with mass
         seg = 63 - __clzll(static_cast<long long>(pos));
         fallback = true;
       }
@@ -1423,22 +1306,22 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
   const double local = ws.smp_target;
   const T* rb = row_ptr<T>(P, P.target, sm.tree, node);
   const T* rs = row_ptr<T>(P, P.draft, sm.tree, node);
-  const Geom g = row_geom(rb, P.vocab);
-  const SegRange r = seg_range(g, seg, num_segments(g));
-  const int nh = r.first ? g.head : 0;
+  const Geom geo = row_geom(rb, P.vocab);
+  const SegRange r = stripe(geo, seg, G);
+  const int nh = r.first ? geo.head : 0;
   const int nv = max(0, r.ve - r.vb);
-  const int nt = r.last ? g.tail : 0;
+  const int nt = r.last ? geo.tail : 0;
   const int nu = nh + nv + nt;
   const int u0 = static_cast<int>((static_cast<long long>(tid) * nu) / kNT);
   const int u1 = static_cast<int>((static_cast<long long>(tid + 1) * nu) / kNT);
   const TermParams tp{sm.smp_cb, sm.smp_cs, sm.smp_ap, sm.smp_bp};
-  const int tail0 = g.head + g.nvec * E;
+  const int tail0 = geo.head + geo.nvec * E;
   auto run = [&](auto two_tag) {
     constexpr bool TWO = decltype(two_tag)::value;
     using TM = Terms<A, TWO, false>;
     const TM tm(ar, tp);
     double unused = 0.0;
-    // element weights of unit i of the segment (a head/tail element or a
+    // element weights of unit i of the stripe (a head/tail element or a
     // vector); returns the count and the first token id
     auto unit = [&](int i, double (&wd)[E], int& tok0) -> int {
       if (i < nh || i >= nh + nv) {
@@ -1449,9 +1332,9 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
       }
       const int v = r.vb + (i - nh);
       float xb[E], xs[E];
-      Elem<T>::unpack(load16(rb, g.head, v), xb);
+      Elem<T>::unpack(load16(rb, geo.head, v), xb);
       if constexpr (TWO) {
-        Elem<T>::unpack(load16(rs, g.head, v), xs);
+        Elem<T>::unpack(load16(rs, geo.head, v), xs);
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) xs[e] = 0.0f;
@@ -1460,7 +1343,7 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
       tm.weights(xb, xs, w, unused);
 #pragma unroll
       for (int e = 0; e < E; ++e) wd[e] = static_cast<double>(w[e]);
-      tok0 = g.head + v * E;
+      tok0 = geo.head + v * E;
       return E;
     };
     // the same unit sums as the pass: fp32 (fast) or fp64 (precise) per unit
@@ -1470,8 +1353,8 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
         return scalar_weight<T, TM, TWO>(tm, rb, rs, x, unused);
       }
       const int v = r.vb + (i - nh);
-      const uint4 vb = load16(rb, g.head, v);
-      const uint4 vs = TWO ? load16(rs, g.head, v) : make_uint4(0, 0, 0, 0);
+      const uint4 vb = load16(rb, geo.head, v);
+      const uint4 vs = TWO ? load16(rs, geo.head, v) : make_uint4(0, 0, 0, 0);
       return vec_sum<T, TM, TWO>(tm, vb, vs, unused);
     };
     double mine = 0.0;
@@ -1519,16 +1402,19 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
   __syncthreads();
 }
 
-// One controller step of the owner (all threads): combine the completed batch,
-// advance the traversal, then publish the next batch or finish the tree.
+// One controller step (all threads; every member of the group runs it on the
+// same data): combine the completed batch, then advance the traversal until it
+// needs the next batch or the tree is done. Only member 0 draws Y.
 template <typename T, class A, int kCap>
-__device__ __attribute__((noinline)) void owner_step(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
-                                                     const Lds<Params>& P, A ar) {
+__device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& sm,
+                                                          Lds<WgScratch>& ws,
+                                                          const Lds<Params>& P, A ar, int g,
+                                                          int m) {
   const int tid = threadIdx.x;
   if (sm.status == TV_TREE_OK) {
     int done_cmd = kCmdNone;
     if (sm.pending) {
-      combine<T, A>(sm, P, ar);
+      combine<T, A>(sm, P, ar, g);
       done_cmd = sm.bcmd[0];
       if (tid == 0) sm.pending = 0;
     }
@@ -1536,198 +1422,92 @@ __device__ __attribute__((noinline)) void owner_step(Lds<TreeSmem<kCap>>& sm, Ld
       if (tid == 0) advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
       __syncthreads();
       if (sm.cmd != kCmdLocalSample) break;
-      local_sample<T, A>(sm, ws, P, ar);
+      if (m == 0) local_sample<T, A>(sm, ws, P, ar, g);
+      else if (tid == 0) sm.res_y = 0;   // Y is reported by member 0
+      __syncthreads();
       done_cmd = kCmdLocalSample;
     }
   } else if (tid == 0) {
     sm.cmd = kCmdDone;
   }
   __syncthreads();
-  if (sm.cmd == kCmdDone) {
-    finish_tree(sm, P);
-    return;
-  }
-  publish<T>(sm, P);
 }
 
-// Claims item `old` of owner slot o's batch if it is valid; the descriptor
-// words were loaded alongside the claim and are reloaded if they belong to an
-// earlier batch. Wavefront 0.
-template <class PP>
-__device__ __forceinline__ bool take_item(Lds<WgScratch>& ws, const PP& P, int o, uint64_t old,
-                                          uint64_t dword, long long t0) {
-  const int lane = threadIdx.x & 63;
-  const Work got = unpack_work(old);
-  if (got.cnt >= got.total) return false;
-  fence_acquire();
-  const uint64_t* g = ws_desc(P, o);
-  for (;;) {
-    const uint64_t seq = __shfl(static_cast<int>(dword & 0x3FFFu), kDescWords - 1, 64);
-    if (static_cast<int>(seq) == got.seq) break;
-    if (lane < kDescWords) dword = ld_rlx(g + lane);
-    if (wall_clock64() - t0 > P.spin_limit) break;
-  }
-  if (lane < kDescWords) ws.item_desc[lane] = dword;
-  if (lane == 0) {
-    ws.item_owner = o;
-    ws.item_word = old;
-  }
-  return true;
-}
-
-// Wavefront 0: waits until this workgroup's batch is complete, it claims a
-// tree or an item of some published batch, or the launch is over.
-template <int kCap>
-__device__ int wait_event(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws, const Params& P) {
-  const int lane = threadIdx.x & 63;
-  const int self = blockIdx.x;
-  const int grid = P.grid;
-  uint64_t* words = ws_words(P);
-  long long t0 = wall_clock64();
-  uint32_t last_rem = 0xFFFFFFFFu;
-  const int rot = (self * 37) & 63;
-  int backoff = 0;
-  for (;;) {
-    if (sm.has_tree) {
-      // An owner works on its own batch only, so that it sees the batch
-      // complete as soon as possible: claim its items, then wait.
-      if (!sm.pending) return kEvOwn;
-      uint64_t old = 0;
-      uint32_t d = 0;
-      if (lane == 0) {
-        const Work wk = unpack_work(ld_rlx(&words[self]));
-        if (wk.cnt < wk.total)
-          old = __hip_atomic_fetch_add(&words[self], 1ull, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        else
-          d = ld_rlx(&ws_done(P)[self]);
+// This member's share of the batch in sm.b* (all threads): its stripe of every
+// pass, then the group exchange. Returns false if the launch was abandoned.
+template <typename T, class A, int kCap>
+__device__ __forceinline__ bool run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
+                                          const Params& P, const A& ar, int g, int m) {
+  const int tid = threadIdx.x;
+  const int bn = sm.bn;
+  const uint32_t seq = sm.seq + 1u;
+  const int par = static_cast<int>(seq & 1u);
+  const int b = sm.tree;
+  for (int p = 0; p < bn; ++p) {
+    const int node = sm.bnode[p];
+    const int cmd = sm.bcmd[p];
+    const T* rb = row_ptr<T>(P, P.target, b, node);
+    const T* rs = row_ptr<T>(P, P.draft, b, node);
+    const Geom geo = row_geom(rb, P.vocab);
+    const SegRange r = stripe(geo, m, P.G);
+    SegPart part;
+    switch (cmd) {
+      case kCmdStats2: stripe_stats<T, A, true>(ws, rb, rs, geo, r, ar, part); break;
+      case kCmdStats1: stripe_stats<T, A, false>(ws, rb, rs, geo, r, ar, part); break;
+      default: {
+        const TermParams tp{sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp};
+        if (cmd == kCmdSPassSd) stripe_wsum<T, A, true>(ws, rb, rs, geo, r, ar, tp, part);
+        else stripe_wsum<T, A, false>(ws, rb, rs, geo, r, ar, tp, part);
+        break;
       }
-      old = shfl_u64(old, 0);
-      d = __shfl(d, 0, 64);
-      const uint64_t dword = lane < kDescWords ? sm.desc[lane] : 0ull;
-      if (old != 0 && take_item(ws, P, self, old, dword, t0)) return kEvItem;
-      if (old == 0 && static_cast<int32_t>(d - sm.expect_done) >= 0) return kEvOwn;
-      if (wall_clock64() - t0 > P.spin_limit) {
-        if (lane == 0) st_rlx(ws_abort(P), 1u);
-        return kEvExit;
-      }
-      continue;
     }
-    if (ws.trees_left) {
-      uint32_t t = 0;
-      if (lane == 0)
-        t = __hip_atomic_fetch_add(ws_next_tree(P), 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-      t = __shfl(t, 0, 64);
-      if (t < static_cast<uint32_t>(P.batch)) {
-        if (lane == 0) ws.new_tree = static_cast<int>(t);
-        return kEvTree;
-      }
-      if (lane == 0) ws.trees_left = 0;
-    }
-    // scan the work words, 64 at a time from a rotating start
-    bool raced = false;
-    const int start = ws.scan_pos;
-    for (int base = 0; base < grid; base += 64) {
-      const int idx = base + lane;
-      int o = start + idx;
-      if (o >= grid) o -= grid;
-      uint64_t w = 0;
-      if (idx < grid) w = ld_rlx(&words[o]);
-      const Work wk = unpack_work(w);
-      const uint64_t avail = __ballot(idx < grid && wk.cnt < wk.total);
-      if (!avail) continue;
-      // one candidate: the k-th available word, k spread by workgroup index, so
-      // that idle workgroups do not all race for the same item
-      const int navail = __popcll(avail);
-      const int k = (self + rot) % navail;
-      const int below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(avail >> 32),
-                                                  __builtin_amdgcn_mbcnt_lo(
-                                                      static_cast<uint32_t>(avail), 0u));
-      const uint64_t pick = __ballot(((avail >> lane) & 1ull) && below == k);
-      const int l = __ffsll(static_cast<long long>(pick)) - 1;
-      const int oc = __shfl(o, l, 64);
-      // the claim and the descriptor loads go out together
-      uint64_t old = 0, dword = 0;
-      if (lane == 0)
-        old = __hip_atomic_fetch_add(&words[oc], 1ull, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
-      else if (lane <= kDescWords)
-        dword = ld_rlx(ws_desc(P, oc) + (lane - 1));
-      old = shfl_u64(old, 0);
-      dword = shfl_u64(dword, (lane + 1) & 63);    // lane i holds word i
-      if (take_item(ws, P, oc, old, dword, t0)) {
-        if (lane == 0) ws.scan_pos = oc;
-        return kEvItem;
-      }
-      raced = true;       // another workgroup took the last item: look again
-      break;
-    }
-    if (raced) continue;
-    uint32_t rem = 0, ab = 0;
-    if (lane == 0) {
-      rem = ld_rlx(ws_remaining(P));
-      ab = ld_rlx(ws_abort(P));
-    }
-    rem = __shfl(rem, 0, 64);
-    ab = __shfl(ab, 0, 64);
-    if (rem == 0 || ab) return kEvExit;
-    const long long now = wall_clock64();
-    if (rem != last_rem) {            // trees are being finished: progress
-      last_rem = rem;
-      t0 = now;
-    } else if (now - t0 > P.spin_limit) {
-      if (lane == 0) st_rlx(ws_abort(P), 1u);
-      return kEvExit;
-    }
-    if (backoff < 8) ++backoff;
-    for (int s = 0; s < backoff; ++s) __builtin_amdgcn_s_sleep(8);
-  }
-}
-
-// A claimed item (all threads): compute its segment's partial result and
-// report it.
-template <typename T, class A>
-__device__ void run_segment(Lds<WgScratch>& ws, const Params& P, const A& ar) {
-  const int o = ws.item_owner;
-  const Work wk = unpack_work(ws.item_word);
-  uint64_t d[kDescWords];
-#pragma unroll
-  for (int i = 0; i < kDescWords; ++i) d[i] = ws.item_desc[i];
-  const int pass = wk.cnt / wk.nseg;
-  const int seg = wk.cnt - pass * wk.nseg;
-  const int node = desc_node(d, pass);
-  const int cmd = desc_cmd(d, pass);
-  const T* rb = row_ptr<T>(P, P.target, wk.tree, node);
-  const T* rs = row_ptr<T>(P, P.draft, wk.tree, node);
-  const Geom g = row_geom(rb, P.vocab);
-  // rows of a batch can differ by one segment (alignment); beyond its last
-  // segment a row contributes an empty partial
-  const SegRange r = seg_range(g, seg, num_segments(g));
-  SegPart part;
-  switch (cmd) {
-    case kCmdStats2: seg_stats<T, A, true>(ws, rb, rs, g, r, ar, part); break;
-    case kCmdStats1: seg_stats<T, A, false>(ws, rb, rs, g, r, ar, part); break;
-    default: {
-      const TermParams tp{__longlong_as_double(static_cast<long long>(d[2])),
-                          __longlong_as_double(static_cast<long long>(d[3])),
-                          __longlong_as_double(static_cast<long long>(d[0])),
-                          __longlong_as_double(static_cast<long long>(d[1]))};
-      if (cmd == kCmdSPassSd) seg_wsum<T, A, true>(ws, rb, rs, g, r, ar, tp, part);
-      else seg_wsum<T, A, false>(ws, rb, rs, g, r, ar, tp, part);
-      break;
+    if (tid == 0) {
+      SegPart* dst = ws_parts(P, g, par, p) + m;
+      st_rlx_f64(&dst->s0, part.s0);
+      st_rlx_f64(&dst->s1, part.s1);
+      st_rlx(reinterpret_cast<uint64_t*>(&dst->m0),
+             (static_cast<uint64_t>(__float_as_uint(part.m1)) << 32) | __float_as_uint(part.m0));
     }
   }
-  if (threadIdx.x == 0) {
-    SegPart* dst = ws_parts(P, o, pass) + seg;
-    st_rlx_f64(&dst->s0, part.s0);
-    st_rlx_f64(&dst->s1, part.s1);
-    st_rlx(reinterpret_cast<uint64_t*>(&dst->m0),
-           (static_cast<uint64_t>(__float_as_uint(part.m1)) << 32) | __float_as_uint(part.m0));
+  if (tid == 0) {
     stores_done();
-    __hip_atomic_fetch_add(&ws_done(P)[o], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(ws_counter(P, g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sm.seq = seq;
+    sm.pending = 1;
+    // the weights of pass 0 stay available for drawing Y at its node
+    const int cmd0 = sm.bcmd[0];
+    sm.spass_node = (cmd0 == kCmdSPass || cmd0 == kCmdSPassSd) ? sm.bnode[0] : -1;
+    sm.last_ap = sm.cmd_ap;
+    sm.last_bp = sm.cmd_bp;
+    sm.last_cb = sm.cmd_cb;
+    sm.last_cs = sm.cmd_cs;
+  }
+  // wait for the other members' partials
+  if (tid < 64) {
+    const uint32_t want = seq * static_cast<uint32_t>(P.G);
+    const long long t0 = wall_clock64();
+    int stop = 0;
+    for (int it = 0;; ++it) {
+      uint32_t c = 0;
+      if (tid == 0) c = ld_rlx(ws_counter(P, g));
+      c = __shfl(c, 0, 64);
+      if (static_cast<int32_t>(c - want) >= 0) break;
+      if ((it & 15) == 15) {
+        uint32_t ab = 0;
+        if (tid == 0) ab = ld_rlx(ws_abort(P));
+        ab = __shfl(ab, 0, 64);
+        if (ab) { stop = 1; break; }
+        if (wall_clock64() - t0 > P.spin_limit) {
+          if (tid == 0) st_rlx(ws_abort(P), 1u);
+          stop = 1;
+          break;
+        }
+      }
+    }
+    if (tid == 0) ws.stop = stop;
   }
   __syncthreads();
+  return !ws.stop;
 }
 
 // ---------------------------------------------------------------------------
@@ -1736,15 +1516,8 @@ __device__ void run_segment(Lds<WgScratch>& ws, const Params& P, const A& ar) {
 
 __global__ void __launch_bounds__(256) init_kernel(Params P) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i == 0) {
-    *ws_remaining(P) = static_cast<uint32_t>(P.batch);
-    *ws_abort(P) = 0u;
-    *ws_next_tree(P) = 0u;
-  }
-  if (i < P.grid) {
-    ws_words(P)[i] = 0ull;
-    ws_done(P)[i] = 0u;
-  }
+  if (i == 0) *ws_abort(P) = 0u;
+  if (i < P.ngroups) *ws_counter(P, i) = 0u;
   if (i < P.batch) {
     P.status[i] = TV_TREE_ABORTED;
     P.accept_len[i] = -1;
@@ -1762,34 +1535,24 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   Lds<WgScratch>& ws = lds_ref(ws_);
   Lds<Params>& Ps = lds_ref(Ps_);
   const int tid = threadIdx.x;
+  const int g = static_cast<int>(blockIdx.x) / P.G;
+  const int m = static_cast<int>(blockIdx.x) - g * P.G;
   if (tid == 0) {
     Ps_ = P;
-    sm.has_tree = 0;
-    sm.pending = 0;
     sm.seq = 0;
-    sm.expect_done = 0;
-    ws.trees_left = 1;
-    ws.scan_pos = static_cast<int>(blockIdx.x);
+    ws.stop = 0;
   }
   __syncthreads();
-  for (;;) {
-    if (tid < 64) {
-      const int ev = wait_event(sm, ws, P);
-      if (tid == 0) ws.event = ev;
+  for (int b = g; b < P.batch; b += P.ngroups) {
+    begin_tree<T>(sm, Ps, b);
+    bool live = true;
+    for (;;) {
+      controller_step<T, A>(sm, ws, Ps, ar, g, m);
+      if (sm.cmd == kCmdDone) break;
+      if (!(live = run_batch<T, A>(sm, ws, P, ar, g, m))) break;
     }
-    __syncthreads();
-    const int ev = ws.event;
-    if (ev == kEvExit) break;
-    // The owner's work (its own items, its controller) is on its tree's
-    // critical path: it gets issue priority over other waves of the CU.
-    if (sm.has_tree || ev != kEvItem) __builtin_amdgcn_s_setprio(2);
-    if (ev == kEvItem) {
-      run_segment<T, A>(ws, P, ar);
-    } else {
-      if (ev == kEvTree) begin_tree<T>(sm, Ps, ws.new_tree);
-      owner_step<T, A>(sm, ws, Ps, ar);
-    }
-    __builtin_amdgcn_s_setprio(0);
+    if (!live) break;
+    if (m == 0) finish_tree(sm, Ps);
   }
 }
 
@@ -1798,7 +1561,7 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
 constexpr int kPreciseBelowVocab = 16384;
 
 template <typename T, class A, int kCap>
-int launch_typed(Params P, const A& ar, int slots, hipStream_t stream) {
+int launch_typed(Params P, A ar, hipStream_t stream) {
   int dev = 0, cus = 0, clock_khz = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return TV_ERR_HIP;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -1808,27 +1571,39 @@ int launch_typed(Params P, const A& ar, int slots, hipStream_t stream) {
       hipSuccess)
     return TV_ERR_HIP;
   if (per_cu < 1) per_cu = 1;
-  // every workgroup spins until the launch is over, so the grid is at most
-  // what can be resident at once; more than one per segment in flight is useless
-  long long grid = static_cast<long long>(per_cu) * (cus > 0 ? cus : 1);
-  if (grid > slots) grid = slots;
-  if (grid < 1) grid = 1;
-  P.grid = static_cast<int>(grid);
-  P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s without progress
-  const int init_n = P.batch > P.grid ? P.batch : P.grid;
-  hipLaunchKernelGGL(init_kernel, dim3((init_n + 255) / 256), dim3(256), 0, stream, P);
+  long long resident = static_cast<long long>(per_cu) * (cus > 0 ? cus : 1);
+  if (resident > tv::kMaxGrid) resident = tv::kMaxGrid;
+  // group size: fill the device, at most kMaxGroup members and no stripe
+  // narrower than 512 vectors
+  const long long nvec = static_cast<long long>(P.vocab) * static_cast<long long>(sizeof(T)) / 16;
+  long long G = resident / P.batch;
+  if (G > kMaxGroup) G = kMaxGroup;
+  if (G > nvec / 512) G = nvec / 512;
+  if (G < 1) G = 1;
+  long long ngroups = resident / G;
+  if (ngroups > P.batch) ngroups = P.batch;
+  P.G = static_cast<int>(G);
+  P.ngroups = static_cast<int>(ngroups);
+  P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s
+  const long long init_n = P.batch > ngroups ? P.batch : ngroups;
+  hipLaunchKernelGGL(init_kernel, dim3(static_cast<unsigned>((init_n + 255) / 256)), dim3(256), 0,
+                     stream, P);
   if (hipGetLastError() != hipSuccess) return TV_ERR_HIP;
-  hipLaunchKernelGGL((verify_kernel<T, A, kCap>), dim3(static_cast<unsigned>(grid)), dim3(kNT),
-                     0, stream, P, ar);
-  return hipGetLastError() == hipSuccess ? TV_OK : TV_ERR_HIP;
+  // cooperative: the members of a group wait for each other, so all of them
+  // must be resident at once
+  void* args[] = {&P, &ar};
+  const hipError_t e = hipLaunchCooperativeKernel(
+      reinterpret_cast<const void*>(verify_kernel<T, A, kCap>),
+      dim3(static_cast<unsigned>(ngroups * G)), dim3(kNT), args, 0, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
 
 template <typename T, int kCap>
-int launch_cap(const Params& P, bool precise, int slots, hipStream_t stream) {
+int launch_cap(const Params& P, bool precise, hipStream_t stream) {
   if constexpr (sizeof(T) == 2) {
-    if (!precise) return launch_typed<T, FastArith, kCap>(P, FastArith{P.k32}, slots, stream);
+    if (!precise) return launch_typed<T, FastArith, kCap>(P, FastArith{P.k32}, stream);
   }
-  return launch_typed<T, PreciseArith, kCap>(P, PreciseArith{P.k64}, slots, stream);
+  return launch_typed<T, PreciseArith, kCap>(P, PreciseArith{P.k64}, stream);
 }
 
 }  // namespace
@@ -1852,11 +1627,8 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   P.p_init = a.p_init;
   P.counters = a.counters;
   P.ws = static_cast<uint8_t*>(workspace);
-  P.off_words = L.off_words;
-  P.off_done = L.off_done;
-  P.off_desc = L.off_desc;
+  P.off_counters = L.off_counters;
   P.off_parts = L.off_parts;
-  P.seg_stride = L.seg_stride;
   P.batch = a.batch;
   P.num_nodes = a.num_nodes;
   P.vocab = a.vocab;
@@ -1867,10 +1639,10 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   const bool precise = a.dtype == TV_DTYPE_F32 || a.vocab < kPreciseBelowVocab;
   const bool small = a.num_nodes <= kCapSmall;
   if (a.dtype == TV_DTYPE_BF16)
-    return small ? launch_cap<uint16_t, kCapSmall>(P, precise, L.slots, stream)
-                 : launch_cap<uint16_t, kCapLarge>(P, precise, L.slots, stream);
-  return small ? launch_cap<float, kCapSmall>(P, true, L.slots, stream)
-               : launch_cap<float, kCapLarge>(P, true, L.slots, stream);
+    return small ? launch_cap<uint16_t, kCapSmall>(P, precise, stream)
+                 : launch_cap<uint16_t, kCapLarge>(P, precise, stream);
+  return small ? launch_cap<float, kCapSmall>(P, true, stream)
+               : launch_cap<float, kCapLarge>(P, true, stream);
 }
 
 }  // namespace tv
