@@ -83,7 +83,10 @@ enum : int {
   kPhDescend = 0, kPhTest, kPhAfterSPass, kPhFinal, kPhFinalLeafStats, kPhFinalWSum,
   kPhAfterSample, kPhPinit, kPhTlVisit, kPhTlAfterSPass
 };
-enum : uint8_t { kFlagStats = 1, kFlagConsulted = 2, kFlagBad = 4, kFlagSd = 8 };
+enum : uint8_t {
+  kFlagStats = 1, kFlagConsulted = 2, kFlagBad = 4, kFlagSd = 8,
+  kFlagPrunedBelow = 16     // children from prune_from on, and their subtrees, are pruned
+};
 
 struct Params {
   const int32_t* parents;
@@ -511,6 +514,56 @@ __device__ __forceinline__ double scalar_weight(const TM& tm, const T* rb, const
   return tm.sum(xb, xs, sd);
 }
 
+// One round of loads: vectors v0 + u * kNT (u < U) of both rows, clamped to
+// vmax so that every load is issued unconditionally.
+template <typename T, bool TWO, int U>
+struct Round {
+  uint4 b[U], s[U];
+  __device__ __forceinline__ void load(const T* rb, const T* rs, int head, int v0, int vmax) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = min(v0 + u * kNT, vmax);
+      b[u] = load16(rb, head, v);
+      if constexpr (TWO) s[u] = load16(rs, head, v);
+    }
+  }
+  __device__ __forceinline__ void pin_all() {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      pin(b[u]);
+      if constexpr (TWO) pin(s[u]);
+    }
+  }
+};
+
+// Calls f(target vector, draft vector) for every vector of the stripe this
+// thread owns (vb + tid + i * kNT), in that order. Each step issues two rounds
+// of loads before any arithmetic and consumes the first round while the
+// second is still in flight. Loads past the stripe are clamped re-reads of its
+// last vector.
+template <typename T, bool TWO, int U, class F>
+__device__ __forceinline__ void stream_stripe(const T* rb, const T* rs, int head,
+                                              const SegRange& r, F&& f) {
+  constexpr int kRound = kNT * U;
+  const int tid = threadIdx.x;
+  const int vmax = r.ve - 1;
+  auto consume = [&](Round<T, TWO, U>& q, int base) {
+    q.pin_all();
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (base + tid + u * kNT < r.ve) f(q.b[u], q.s[u]);
+  };
+#pragma unroll 1
+  for (int base = r.vb; base < r.ve; base += 2 * kRound) {
+    Round<T, TWO, U> x, y;
+    x.load(rb, rs, head, base + tid, vmax);
+    y.load(rb, rs, head, base + kRound + tid, vmax);
+    __builtin_amdgcn_sched_barrier(0);
+    consume(x, base);
+    consume(y, base + kRound);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Stripe passes. Thread t takes vectors vb + t + i * kNT of the stripe; per
 // thread: head elements, vectors in order, tail elements. Loads are
@@ -522,7 +575,6 @@ template <typename T, class A, bool TWO>
 __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
                              const SegRange& r, const A& ar, SegPart& out) {
   constexpr int E = Elem<T>::E;
-  constexpr int kUnroll = kUnrollOf<A>;
   const int tid = threadIdx.x;
   Online ob = online_init(ar), os = online_init(ar);
   if (r.first && tid < g.head) {
@@ -533,33 +585,15 @@ __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const
       online_add(os, xs, ar);
     }
   }
-#pragma unroll 1
-  for (int base = r.vb; base < r.ve; base += kNT * kUnroll) {
-    uint4 lb[kUnroll], ls[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int v = min(base + tid + u * kNT, r.ve - 1);
-      lb[u] = load16(rb, g.head, v);
-      if constexpr (TWO) ls[u] = load16(rs, g.head, v);
+  stream_stripe<T, TWO, kUnrollOf<A>>(rb, rs, g.head, r, [&](const uint4& vb, const uint4& vs) {
+    float x[E];
+    Elem<T>::unpack(vb, x);
+    online_add(ob, x, ar);
+    if constexpr (TWO) {
+      Elem<T>::unpack(vs, x);
+      online_add(os, x, ar);
     }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      pin(lb[u]);
-      if constexpr (TWO) pin(ls[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      if (base + tid + u * kNT < r.ve) {
-        float x[E];
-        Elem<T>::unpack(lb[u], x);
-        online_add(ob, x, ar);
-        if constexpr (TWO) {
-          Elem<T>::unpack(ls[u], x);
-          online_add(os, x, ar);
-        }
-      }
-    }
-  }
+  });
   if (r.last && tid < g.tail) {
     const int i = g.head + g.nvec * E + tid;
     float xb[1] = {Elem<T>::scalar(rb + i)};
@@ -586,30 +620,14 @@ __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const
 template <typename T, class A, bool SD>
 __device__ void stripe_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
                             const SegRange& r, const A& ar, const TermParams& p, SegPart& out) {
-  constexpr int kUnroll = kUnrollOf<A>;
   const Terms<A, true, SD> tm(ar, p);
   using TM = Terms<A, true, SD>;
   const int tid = threadIdx.x;
   double acc = 0.0, sd = 0.0;
   if (r.first && tid < g.head) acc += scalar_weight<T, TM, true>(tm, rb, rs, tid, sd);
-#pragma unroll 1
-  for (int base = r.vb; base < r.ve; base += kNT * kUnroll) {
-    uint4 lb[kUnroll], ls[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int v = min(base + tid + u * kNT, r.ve - 1);
-      lb[u] = load16(rb, g.head, v);
-      ls[u] = load16(rs, g.head, v);
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      pin(lb[u]);
-      pin(ls[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-      if (base + tid + u * kNT < r.ve) acc += vec_sum<T, TM, true>(tm, lb[u], ls[u], sd);
-  }
+  stream_stripe<T, true, kUnrollOf<A>>(rb, rs, g.head, r, [&](const uint4& vb, const uint4& vs) {
+    acc += vec_sum<T, TM, true>(tm, vb, vs, sd);
+  });
   if (r.last && tid < g.tail)
     acc += scalar_weight<T, TM, true>(tm, rb, rs, g.head + g.nvec * Elem<T>::E + tid, sd);
   block_sum2(ws, acc, sd);
@@ -631,6 +649,8 @@ struct TreeSmem {
   int16_t child_start[kCap];
   int16_t child_list[kCap];
   int16_t next_child[kCap];        // children already removed (always a prefix)
+  int16_t rank[kCap];              // position among the parent's children
+  int16_t prune_from[kCap];        // with kFlagPrunedBelow: first pruned child
   int32_t child_count[kCap];
   int32_t token[kCap];
   float u[kCap];
@@ -841,6 +861,16 @@ __device__ __forceinline__ void advance_impl(Lds<TreeSmem<kCap>>& sm, TraversalA
       // ---- Traversal Verification ----------------------------------------
       case kPhDescend: {   // walk to the first leaf of the remaining tree
         const int j = ct.cur;
+        if (sm.next_child[j] < sm.child_count[j] && sm.pi[j] == 0.0) {
+          // every chain through j has rate 0: the remaining children and their
+          // subtrees are pruned without visiting them (their outputs are
+          // written when the tree finishes), and j itself is tested next
+          sm.prune_from[j] = sm.next_child[j];
+          sm.flags[j] |= kFlagPrunedBelow;
+          sm.next_child[j] = static_cast<int16_t>(sm.child_count[j]);
+          ct.phase = kPhTest;
+          continue;
+        }
         if (sm.next_child[j] < sm.child_count[j]) {
           if (sm.pi[j] > 0.0) {
             if (!(sm.flags[j] & kFlagConsulted)) {
@@ -1097,6 +1127,7 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, co
       for (int k2 = 1; k2 < i; ++k2) rank += (sm.parent[k2] == p);
       for (int a = p; a > 0; a = sm.parent[a]) ++d;
       sm.child_list[sm.child_start[p] + rank] = static_cast<int16_t>(i);
+      sm.rank[i] = static_cast<int16_t>(rank);
       sm.depth[i] = static_cast<int16_t>(d);
     }
     if (tid == 0) sm.depth[0] = 0;
@@ -1148,6 +1179,19 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
   const int n1 = P.num_nodes;
   const size_t tree_off = static_cast<size_t>(b) * n1;
   const bool ok = sm.status == TV_TREE_OK;
+  // nodes below a chain of rate 0 that the traversal skipped
+  for (int i = 1 + tid; i < n1; i += kNT) {
+    if (sm.state[i] != TV_NODE_UNTESTED) continue;
+    for (int x = i; x > 0; x = sm.parent[x]) {
+      const int a = sm.parent[x];
+      if ((sm.flags[a] & kFlagPrunedBelow) && sm.rank[x] >= sm.prune_from[a]) {
+        sm.state[i] = TV_NODE_PRUNED;
+        sm.theta[i] = 0.0f;
+        break;
+      }
+    }
+  }
+  __syncthreads();
   for (int i = tid; i < n1; i += kNT) {
     if (P.node_state) P.node_state[tree_off + i] = ok ? static_cast<int8_t>(sm.state[i]) : 0;
     if (P.node_theta) P.node_theta[tree_off + i] = ok ? sm.theta[i] : -1.0f;
@@ -1236,12 +1280,12 @@ __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
     const int node = sm.bnode[p];
     if (sm.bcmd[p] != kCmdStats2 || (sm.flags[node] & kFlagBad)) continue;
     const double Cb = sm.cb[node], Cs = sm.cs[node];
-    const double lsb = -log2(sm.invsb[node]), lss = -log2(sm.invss[node]);
+    const double norm = sm.invsb[node] / sm.invss[node];   // ts / tb
     for (int i = tid; i < sm.child_count[node]; i += kNT) {
       const int c = sm.child_list[sm.child_start[node] + i];
-      const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb) - lsb;
-      const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs) - lss;
-      sm.r0[c] = exp2(lp - lq);
+      const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb);
+      const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs);
+      sm.r0[c] = exp2(lp - lq) * norm;
       sm.et[c] = ar.ex(sm.gs[c], Cs);
       if (sm.gs[c] == -INFINITY) sm.flags[node] |= kFlagBad;   // a token the draft cannot produce
     }
@@ -1419,7 +1463,11 @@ __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& s
       if (tid == 0) sm.pending = 0;
     }
     for (;;) {
-      if (tid == 0) advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
+      if (tid == 0) {
+        __builtin_amdgcn_s_setprio(3);
+        advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
+        __builtin_amdgcn_s_setprio(0);
+      }
       __syncthreads();
       if (sm.cmd != kCmdLocalSample) break;
       if (m == 0) local_sample<T, A>(sm, ws, P, ar, g);
