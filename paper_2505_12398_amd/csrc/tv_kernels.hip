@@ -68,12 +68,9 @@ constexpr int kNT = 256;                       // threads per workgroup
 constexpr int kNW = kNT / 64;
 // vectors per row in flight per lane: the fp64 element path needs more registers
 template <class A> constexpr int kUnrollOf = A::kPrecise ? 2 : 4;
-// Node capacities of the kernel variants and the trees a workgroup holds at once.
-constexpr int kCapSmall = 80, kSlotsSmall = tv::kMaxSlots;
-constexpr int kCapMid = 256, kSlotsMid = 1;
-constexpr int kCapLarge = TV_MAX_NODES, kSlotsLarge = 1;
-constexpr int kMaxBatch = tv::kMaxBatchPasses; // passes per batch of one tree
-constexpr int kMaxGroupPasses = tv::kMaxGroupPasses;
+constexpr int kCapSmall = 128;                 // node capacity of the compact variant
+constexpr int kCapLarge = TV_MAX_NODES;
+constexpr int kMaxBatch = tv::kMaxBatchPasses; // passes per batch
 constexpr int kMaxGroup = tv::kMaxGroup;       // workgroups per tree
 static_assert(kMaxGroup <= 64, "member partials are combined by one wavefront");
 
@@ -113,9 +110,8 @@ struct Params {
   int vocab;
   int mode;
   int algo;
-  int G;                     // workgroups per group
+  int G;                     // workgroups per group (per tree)
   int ngroups;               // groups; group g verifies trees g, g + ngroups, ...
-  int K;                     // trees a group verifies at once
   float k32;                 // log2(e) / T rounded to fp32 (fast element path)
   double k64;                // log2(e) / T (precise element path)
 };
@@ -152,7 +148,7 @@ __device__ __forceinline__ uint32_t* ws_counter(const PP& P, int g) {
 template <class PP>
 __device__ __forceinline__ SegPart* ws_parts(const PP& P, int g, int par, int p) {
   return reinterpret_cast<SegPart*>(P.ws + P.off_parts) +
-         ((static_cast<size_t>(g) * 2 + par) * kMaxGroupPasses + p) * P.G;
+         ((static_cast<size_t>(g) * 2 + par) * kMaxBatch + p) * P.G;
 }
 
 __device__ __forceinline__ uint64_t ld_rlx(const uint64_t* p) {
@@ -689,6 +685,8 @@ struct TreeSmem {
   int8_t bcmd[kMaxBatch];
   double cmd_ap, cmd_bp, cmd_cb, cmd_cs;    // parameters of a SPASS / WSUM pass 0
   // the batch in flight, then just completed
+  int pending;
+  uint32_t seq;                    // batches this group has run (all trees so far)
   int spass_node;                  // node whose SPASS partials are in the workspace (-1: none)
   double last_ap, last_bp, last_cb, last_cs;
   // local sample request
@@ -1163,6 +1161,7 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, co
     init_node_state(sm, 0, 1.0);
     sm.res_y = -1;
     sm.cmd = kCmdNone;
+    sm.pending = 0;
     sm.spass_node = -1;
     const bool tv_algo = P.algo == static_cast<int>(tv::Algo::kTraversal);
     if (P.p_init && tv_algo) sm.phase = kPhPinit;
@@ -1210,6 +1209,7 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
       c[2] = ok ? (sm.child_count[sm.accepted] == 0 ? 1 : 0) : 0;
       c[3] = ok ? sm.tests : 0;
     }
+    sm.has_tree = 0;
   }
   __syncthreads();
 }
@@ -1218,19 +1218,93 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
 // Group exchange: combining the members' partials, the local sample
 // ---------------------------------------------------------------------------
 
+// Combines the members' partials of the completed batch (all threads): wave w
+// takes passes w, w + 4, lanes are members; STATS results go to the node
+// arrays, a SPASS / WSUM result to res_S / res_sd.
+template <typename T, class A, int kCap>
+__device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
+                                                       const Lds<Params>& P, A ar, int g) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bn = sm.bn;
+  const int G = P.G;
+  const int par = static_cast<int>(sm.seq & 1u);
+  fence_acquire();
+  for (int p = wave; p < bn; p += kNW) {
+    const int cmd = sm.bcmd[p];
+    const int node = sm.bnode[p];
+    const SegPart* part = ws_parts(P, g, par, p);
+    double s0 = 0.0, s1 = 0.0;
+    float m0 = -INFINITY, m1 = -INFINITY;
+    if (lane < G) {
+      s0 = ld_rlx_f64(&part[lane].s0);
+      s1 = ld_rlx_f64(&part[lane].s1);
+      const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
+      m0 = __uint_as_float(static_cast<uint32_t>(mm));
+      m1 = __uint_as_float(static_cast<uint32_t>(mm >> 32));
+    }
+    if (cmd == kCmdStats2 || cmd == kCmdStats1) {
+      const bool two = cmd == kCmdStats2;
+      const float Mb = wave_max(m0);
+      const float Ms = two ? wave_max(m1) : -INFINITY;
+      const double Cb = ar.frame(Mb);
+      const double Cs = two ? ar.frame(Ms) : 0.0;
+      // stripe sums in the row's frame; a stripe with no finite value adds 0 (or NaN)
+      double tb = (m0 > -INFINITY) ? s0 * exp2(Cb - ar.frame(m0)) : s0;
+      double ts = two ? ((m1 > -INFINITY) ? s1 * exp2(Cs - ar.frame(m1)) : s1) : 0.0;
+      tb = __shfl(wave_sum(tb), 0, 64);
+      ts = __shfl(wave_sum(ts), 0, 64);
+      if (lane == 0) {
+        const bool bad = !(Mb > -INFINITY) || !isfinite(tb) ||
+                         (two && (!(Ms > -INFINITY) || !isfinite(ts)));
+        sm.cb[node] = Cb;
+        sm.invsb[node] = 1.0 / tb;
+        if (two) {
+          sm.cs[node] = Cs;
+          sm.invss[node] = 1.0 / ts;
+        }
+        sm.flags[node] |= kFlagStats | (bad ? kFlagBad : 0);
+      }
+    } else {
+      const double S = __shfl(wave_sum(s0), 0, 64);
+      const double sd = __shfl(wave_sum(s1), 0, 64);
+      if (lane == 0) {
+        sm.res_S = S;
+        sm.res_sd = sd;
+      }
+    }
+  }
+  __syncthreads();
+  // children's original ratios r0 = p(x)/q(x) and draft terms
+  const double kd = ar.kd();
+  for (int p = 0; p < bn; ++p) {
+    const int node = sm.bnode[p];
+    if (sm.bcmd[p] != kCmdStats2 || (sm.flags[node] & kFlagBad)) continue;
+    const double Cb = sm.cb[node], Cs = sm.cs[node];
+    const double norm = sm.invsb[node] / sm.invss[node];   // ts / tb
+    for (int i = tid; i < sm.child_count[node]; i += kNT) {
+      const int c = sm.child_list[sm.child_start[node] + i];
+      const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb);
+      const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs);
+      sm.r0[c] = exp2(lp - lq) * norm;
+      sm.et[c] = ar.ex(sm.gs[c], Cs);
+      if (sm.gs[c] == -INFINITY) sm.flags[node] |= kFlagBad;   // a token the draft cannot produce
+    }
+  }
+  __syncthreads();
+}
+
 // Inverse-CDF draw of Y (all threads of one member). The weights of the
 // stripes come from the partials of pass 0 of the batch just completed; the
 // stripe holding u*W is rescanned.
 template <typename T, class A, int kCap>
 __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
-                                                       const Lds<Params>& P, A ar, int g,
-                                                       uint32_t seq, int q0) {
+                                                       const Lds<Params>& P, A ar, int g) {
   constexpr int E = Elem<T>::E;
   const int tid = threadIdx.x, lane = tid & 63;
   const int node = sm.bnode[0];
   const int G = P.G;
   if (tid < 64) {
-    const SegPart* part = ws_parts(P, g, static_cast<int>(seq & 1u), q0);
+    const SegPart* part = ws_parts(P, g, static_cast<int>(sm.seq & 1u), 0);
     double w = 0.0;
     if (lane < G) {
       const double s0 = ld_rlx_f64(&part[lane].s0);
@@ -1372,212 +1446,54 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
   __syncthreads();
 }
 
-// ---------------------------------------------------------------------------
-// A group's trees in flight. A group verifies up to K trees at once, one per
-// slot; each group batch is the concatenation, in slot order, of the batches
-// the slots' traversals asked for.
-// ---------------------------------------------------------------------------
-
-template <int kCap, int kK>
-struct GroupSmem {
-  TreeSmem<kCap> t[kK];
-  uint32_t seq;                        // group batches run so far
-  int np;                              // passes of the current group batch
-  int next_tree;                       // next tree of this group not yet started
-  int8_t qslot[kK * kMaxBatch];        // slot and position of each pass of the batch
-  int8_t qpos[kK * kMaxBatch];
-  int8_t boff[kK];                     // first pass of each slot in the batch (-1: none)
-  int8_t adv[kK];                      // the slot's traversal has a result to consume
-  int8_t adv_cmd[kK];                  // the kind of that result
-};
-
-// Starts the group's next tree in slot k, if any is left (all threads). The
-// first barrier makes every thread finish reading the slot's state (the
-// caller's loop tests has_tree and cmd) before thread 0 changes it: a thread
-// that read has_tree after the change would skip this call and its barriers.
-template <typename T, int kCap, int kK>
-__device__ __forceinline__ void start_slot(Lds<GroupSmem<kCap, kK>>& gs, const Lds<Params>& P,
-                                           int k) {
-  __syncthreads();
-  const int b = gs.next_tree;
-  if (b < P.batch) {
-    begin_tree<T>(gs.t[k], P, b);
-    if (threadIdx.x == 0) {
-      gs.next_tree = b + P.ngroups;
-      gs.adv[k] = 1;
-      gs.adv_cmd[k] = kCmdNone;
+// One controller step (all threads; every member of the group runs it on the
+// same data): combine the completed batch, then advance the traversal until it
+// needs the next batch or the tree is done. Only member 0 draws Y.
+template <typename T, class A, int kCap>
+__device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& sm,
+                                                          Lds<WgScratch>& ws,
+                                                          const Lds<Params>& P, A ar, int g,
+                                                          int m) {
+  const int tid = threadIdx.x;
+  if (sm.status == TV_TREE_OK) {
+    int done_cmd = kCmdNone;
+    if (sm.pending) {
+      combine<T, A>(sm, P, ar, g);
+      done_cmd = sm.bcmd[0];
+      if (tid == 0) sm.pending = 0;
     }
-  } else if (threadIdx.x == 0) {
-    gs.t[k].has_tree = 0;
-    gs.adv[k] = 0;
-  }
-  __syncthreads();
-}
-
-// Combines the members' partials of the completed group batch (all threads):
-// wave w takes passes w, w + 4, ..., lanes are members; STATS results go to
-// the node arrays, a SPASS / WSUM result to the slot's res_S / res_sd.
-template <typename T, class A, int kCap, int kK>
-__device__ __forceinline__ void combine(Lds<GroupSmem<kCap, kK>>& gs, const Lds<Params>& P,
-                                        A ar, int g) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int np = gs.np;
-  const int G = P.G;
-  const int par = static_cast<int>(gs.seq & 1u);
-  fence_acquire();
-  for (int q = wave; q < np; q += kNW) {
-    Lds<TreeSmem<kCap>>& sm = gs.t[gs.qslot[q]];
-    const int p = gs.qpos[q];
-    const int cmd = sm.bcmd[p];
-    const int node = sm.bnode[p];
-    const SegPart* part = ws_parts(P, g, par, q);
-    double s0 = 0.0, s1 = 0.0;
-    float m0 = -INFINITY, m1 = -INFINITY;
-    if (lane < G) {
-      s0 = ld_rlx_f64(&part[lane].s0);
-      s1 = ld_rlx_f64(&part[lane].s1);
-      const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
-      m0 = __uint_as_float(static_cast<uint32_t>(mm));
-      m1 = __uint_as_float(static_cast<uint32_t>(mm >> 32));
-    }
-    if (cmd == kCmdStats2 || cmd == kCmdStats1) {
-      const bool two = cmd == kCmdStats2;
-      const float Mb = wave_max(m0);
-      const float Ms = two ? wave_max(m1) : -INFINITY;
-      const double Cb = ar.frame(Mb);
-      const double Cs = two ? ar.frame(Ms) : 0.0;
-      // stripe sums in the row's frame; a stripe with no finite value adds 0 (or NaN)
-      double tb = (m0 > -INFINITY) ? s0 * exp2(Cb - ar.frame(m0)) : s0;
-      double ts = two ? ((m1 > -INFINITY) ? s1 * exp2(Cs - ar.frame(m1)) : s1) : 0.0;
-      tb = __shfl(wave_sum(tb), 0, 64);
-      ts = __shfl(wave_sum(ts), 0, 64);
-      if (lane == 0) {
-        const bool bad = !(Mb > -INFINITY) || !isfinite(tb) ||
-                         (two && (!(Ms > -INFINITY) || !isfinite(ts)));
-        sm.cb[node] = Cb;
-        sm.invsb[node] = 1.0 / tb;
-        if (two) {
-          sm.cs[node] = Cs;
-          sm.invss[node] = 1.0 / ts;
-        }
-        sm.flags[node] |= kFlagStats | (bad ? kFlagBad : 0);
-      }
-    } else {
-      const double S = __shfl(wave_sum(s0), 0, 64);
-      const double sd = __shfl(wave_sum(s1), 0, 64);
-      if (lane == 0) {
-        sm.res_S = S;
-        sm.res_sd = sd;
-      }
-    }
-  }
-  __syncthreads();
-  // children's original ratios r0 = p(x)/q(x) and draft terms (8 threads per pass)
-  const double kd = ar.kd();
-  for (int q = tid >> 3; q < np; q += kNT / 8) {
-    Lds<TreeSmem<kCap>>& sm = gs.t[gs.qslot[q]];
-    const int p = gs.qpos[q];
-    const int node = sm.bnode[p];
-    if (sm.bcmd[p] != kCmdStats2 || (sm.flags[node] & kFlagBad)) continue;
-    const double Cb = sm.cb[node], Cs = sm.cs[node];
-    const double norm = sm.invsb[node] / sm.invss[node];   // ts / tb
-    for (int i = tid & 7; i < sm.child_count[node]; i += 8) {
-      const int c = sm.child_list[sm.child_start[node] + i];
-      const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb);
-      const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs);
-      sm.r0[c] = exp2(lp - lq) * norm;
-      sm.et[c] = ar.ex(sm.gs[c], Cs);
-      if (sm.gs[c] == -INFINITY) sm.flags[node] |= kFlagBad;   // a token the draft cannot produce
-    }
-  }
-  if (tid < kK && gs.boff[tid] >= 0) {
-    gs.adv[tid] = 1;
-    gs.adv_cmd[tid] = gs.t[tid].bcmd[0];
-  }
-  __syncthreads();
-}
-
-// One controller phase (all threads; every member of the group runs it on the
-// same data): combine the completed group batch, advance the traversals that
-// have new results (one wave per slot) until each needs its next batch or is
-// done, draw Y where asked (member 0), finish trees and start the next ones,
-// and lay out the next group batch.
-template <typename T, class A, int kCap, int kK>
-__device__ __attribute__((noinline)) void group_controller(Lds<GroupSmem<kCap, kK>>& gs,
-                                                           Lds<WgScratch>& ws,
-                                                           const Lds<Params>& P, A ar, int g,
-                                                           int m) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (gs.np > 0) combine<T, A>(gs, P, ar, g);
-  for (;;) {
-    if (lane == 0 && wave < kK && gs.adv[wave]) {
-      Lds<TreeSmem<kCap>>& sm = gs.t[wave];
-      if (sm.status == TV_TREE_OK) {
+    for (;;) {
+      if (tid == 0) {
         __builtin_amdgcn_s_setprio(3);
-        advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, gs.adv_cmd[wave]);
+        advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
         __builtin_amdgcn_s_setprio(0);
-      } else {
-        sm.cmd = kCmdDone;
       }
-      gs.adv[wave] = 0;
+      __syncthreads();
+      if (sm.cmd != kCmdLocalSample) break;
+      if (m == 0) local_sample<T, A>(sm, ws, P, ar, g);
+      else if (tid == 0) sm.res_y = 0;   // Y is reported by member 0
+      __syncthreads();
+      done_cmd = kCmdLocalSample;
     }
-    __syncthreads();
-    bool again = false;
-    for (int k = 0; k < kK; ++k) {
-      Lds<TreeSmem<kCap>>& sm = gs.t[k];
-      if (!sm.has_tree) continue;
-      if (sm.cmd == kCmdLocalSample) {
-        if (m == 0) local_sample<T, A>(sm, ws, P, ar, g, gs.seq, gs.boff[k]);
-        else if (tid == 0) sm.res_y = 0;   // Y is reported by member 0
-        if (tid == 0) {
-          gs.adv[k] = 1;
-          gs.adv_cmd[k] = kCmdLocalSample;
-        }
-        __syncthreads();
-        again = true;
-      } else if (sm.cmd == kCmdDone) {
-        if (m == 0) finish_tree(sm, P);
-        start_slot<T>(gs, P, k);
-        again = again || gs.adv[k];
-      }
-    }
-    if (!again) break;
-  }
-  if (tid == 0) {
-    int np = 0;
-    for (int k = 0; k < kK; ++k) {
-      Lds<TreeSmem<kCap>>& sm = gs.t[k];
-      if (sm.has_tree && sm.cmd == kCmdBatch) {
-        gs.boff[k] = static_cast<int8_t>(np);
-        for (int p = 0; p < sm.bn; ++p) {
-          gs.qslot[np] = static_cast<int8_t>(k);
-          gs.qpos[np] = static_cast<int8_t>(p);
-          ++np;
-        }
-      } else {
-        gs.boff[k] = -1;
-      }
-    }
-    gs.np = np;
+  } else if (tid == 0) {
+    sm.cmd = kCmdDone;
   }
   __syncthreads();
 }
 
-// This member's share of the group batch (all threads): its stripe of every
+// This member's share of the batch in sm.b* (all threads): its stripe of every
 // pass, then the group exchange. Returns false if the launch was abandoned.
-template <typename T, class A, int kCap, int kK>
-__device__ __forceinline__ bool run_batch(Lds<GroupSmem<kCap, kK>>& gs, Lds<WgScratch>& ws,
+template <typename T, class A, int kCap>
+__device__ __forceinline__ bool run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
                                           const Params& P, const A& ar, int g, int m) {
   const int tid = threadIdx.x;
-  const int np = gs.np;
-  const uint32_t seq = gs.seq + 1u;
+  const int bn = sm.bn;
+  const uint32_t seq = sm.seq + 1u;
   const int par = static_cast<int>(seq & 1u);
-  for (int q = 0; q < np; ++q) {
-    Lds<TreeSmem<kCap>>& sm = gs.t[gs.qslot[q]];
-    const int p = gs.qpos[q];
+  const int b = sm.tree;
+  for (int p = 0; p < bn; ++p) {
     const int node = sm.bnode[p];
     const int cmd = sm.bcmd[p];
-    const int b = sm.tree;
     const T* rb = row_ptr<T>(P, P.target, b, node);
     const T* rs = row_ptr<T>(P, P.draft, b, node);
     const Geom geo = row_geom(rb, P.vocab);
@@ -1594,7 +1510,7 @@ __device__ __forceinline__ bool run_batch(Lds<GroupSmem<kCap, kK>>& gs, Lds<WgSc
       }
     }
     if (tid == 0) {
-      SegPart* dst = ws_parts(P, g, par, q) + m;
+      SegPart* dst = ws_parts(P, g, par, p) + m;
       st_rlx_f64(&dst->s0, part.s0);
       st_rlx_f64(&dst->s1, part.s1);
       st_rlx(reinterpret_cast<uint64_t*>(&dst->m0),
@@ -1604,18 +1520,15 @@ __device__ __forceinline__ bool run_batch(Lds<GroupSmem<kCap, kK>>& gs, Lds<WgSc
   if (tid == 0) {
     stores_done();
     __hip_atomic_fetch_add(ws_counter(P, g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    gs.seq = seq;
-    for (int k = 0; k < kK; ++k) {
-      if (gs.boff[k] < 0) continue;
-      Lds<TreeSmem<kCap>>& sm = gs.t[k];
-      // the weights of the slot's pass 0 stay available for drawing Y at its node
-      const int cmd0 = sm.bcmd[0];
-      sm.spass_node = (cmd0 == kCmdSPass || cmd0 == kCmdSPassSd) ? sm.bnode[0] : -1;
-      sm.last_ap = sm.cmd_ap;
-      sm.last_bp = sm.cmd_bp;
-      sm.last_cb = sm.cmd_cb;
-      sm.last_cs = sm.cmd_cs;
-    }
+    sm.seq = seq;
+    sm.pending = 1;
+    // the weights of pass 0 stay available for drawing Y at its node
+    const int cmd0 = sm.bcmd[0];
+    sm.spass_node = (cmd0 == kCmdSPass || cmd0 == kCmdSPassSd) ? sm.bnode[0] : -1;
+    sm.last_ap = sm.cmd_ap;
+    sm.last_bp = sm.cmd_bp;
+    sm.last_cb = sm.cmd_cb;
+    sm.last_cs = sm.cmd_cs;
   }
   // wait for the other members' partials
   if (tid < 64) {
@@ -1661,13 +1574,12 @@ __global__ void __launch_bounds__(256) init_kernel(Params P) {
   }
 }
 
-template <typename T, class A, int kCap, int kK>
+template <typename T, class A, int kCap>
 __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
-  static_assert(kK <= kNW, "one wave advances each slot");
-  __shared__ GroupSmem<kCap, kK> gs_;
+  __shared__ TreeSmem<kCap> sm_;
   __shared__ WgScratch ws_;
   __shared__ Params Ps_;     // for the controller, which is not inlined
-  Lds<GroupSmem<kCap, kK>>& gs = lds_ref(gs_);
+  Lds<TreeSmem<kCap>>& sm = lds_ref(sm_);
   Lds<WgScratch>& ws = lds_ref(ws_);
   Lds<Params>& Ps = lds_ref(Ps_);
   const int tid = threadIdx.x;
@@ -1675,23 +1587,20 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   const int m = static_cast<int>(blockIdx.x) - g * P.G;
   if (tid == 0) {
     Ps_ = P;
-    gs.seq = 0;
-    gs.np = 0;
-    gs.next_tree = g;
+    sm.seq = 0;
     ws.stop = 0;
-    for (int k = 0; k < kK; ++k) {
-      gs.t[k].has_tree = 0;
-      gs.adv[k] = 0;
-      gs.boff[k] = -1;
-    }
   }
   __syncthreads();
-  const int K = P.K < kK ? P.K : kK;
-  for (int k = 0; k < K; ++k) start_slot<T>(gs, Ps, k);
-  for (;;) {
-    group_controller<T, A>(gs, ws, Ps, ar, g, m);
-    if (gs.np == 0) break;
-    if (!run_batch<T, A>(gs, ws, P, ar, g, m)) break;
+  for (int b = g; b < P.batch; b += P.ngroups) {
+    begin_tree<T>(sm, Ps, b);
+    bool live = true;
+    for (;;) {
+      controller_step<T, A>(sm, ws, Ps, ar, g, m);
+      if (sm.cmd == kCmdDone) break;
+      if (!(live = run_batch<T, A>(sm, ws, P, ar, g, m))) break;
+    }
+    if (!live) break;
+    if (m == 0) finish_tree(sm, Ps);
   }
 }
 
@@ -1699,38 +1608,30 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
 // with few elements the per-element rounding of the fast path does not average.
 constexpr int kPreciseBelowVocab = 16384;
 
-template <typename T, class A, int kCap, int kK>
+template <typename T, class A, int kCap>
 int launch_typed(Params P, A ar, hipStream_t stream) {
   int dev = 0, cus = 0, clock_khz = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return TV_ERR_HIP;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
     return TV_ERR_HIP;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, verify_kernel<T, A, kCap, kK>, kNT,
-                                                    0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, verify_kernel<T, A, kCap>, kNT, 0) !=
+      hipSuccess)
     return TV_ERR_HIP;
   if (per_cu < 1) per_cu = 1;
   long long resident = static_cast<long long>(per_cu) * (cus > 0 ? cus : 1);
   if (resident > tv::kMaxGrid) resident = tv::kMaxGrid;
-  // Groups of G members verifying K trees at once. A group stripe is at least
-  // 512 vectors and a group has at most kMaxGroup members. K grows with the
-  // batch until the trees in flight fill the device at the widest groups:
-  // more trees per group means the members of a group whose other trees are
-  // done all work on the trees left, instead of waiting for them.
+  // group size: fill the device, at most kMaxGroup members and no stripe
+  // narrower than 512 vectors
   const long long nvec = static_cast<long long>(P.vocab) * static_cast<long long>(sizeof(T)) / 16;
-  long long gmax = nvec / 512 < kMaxGroup ? nvec / 512 : kMaxGroup;
-  if (gmax < 1) gmax = 1;
-  long long K = static_cast<long long>(P.batch) * gmax / resident;
-  if (K > kK) K = kK;
-  if (K < 1) K = 1;
-  long long ngroups = (P.batch + K - 1) / K;
-  if (ngroups > resident) ngroups = resident;
-  long long G = resident / ngroups;
-  if (G > gmax) G = gmax;
+  long long G = resident / P.batch;
+  if (G > kMaxGroup) G = kMaxGroup;
+  if (G > nvec / 512) G = nvec / 512;
   if (G < 1) G = 1;
+  long long ngroups = resident / G;
+  if (ngroups > P.batch) ngroups = P.batch;
   P.G = static_cast<int>(G);
   P.ngroups = static_cast<int>(ngroups);
-  P.K = static_cast<int>(K);
   P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s
   const long long init_n = P.batch > ngroups ? P.batch : ngroups;
   hipLaunchKernelGGL(init_kernel, dim3(static_cast<unsigned>((init_n + 255) / 256)), dim3(256), 0,
@@ -1740,24 +1641,17 @@ int launch_typed(Params P, A ar, hipStream_t stream) {
   // must be resident at once
   void* args[] = {&P, &ar};
   const hipError_t e = hipLaunchCooperativeKernel(
-      reinterpret_cast<const void*>(verify_kernel<T, A, kCap, kK>),
+      reinterpret_cast<const void*>(verify_kernel<T, A, kCap>),
       dim3(static_cast<unsigned>(ngroups * G)), dim3(kNT), args, 0, stream);
   return e == hipSuccess ? TV_OK : TV_ERR_HIP;
 }
 
-template <typename T, int kCap, int kK>
+template <typename T, int kCap>
 int launch_cap(const Params& P, bool precise, hipStream_t stream) {
   if constexpr (sizeof(T) == 2) {
-    if (!precise) return launch_typed<T, FastArith, kCap, kK>(P, FastArith{P.k32}, stream);
+    if (!precise) return launch_typed<T, FastArith, kCap>(P, FastArith{P.k32}, stream);
   }
-  return launch_typed<T, PreciseArith, kCap, kK>(P, PreciseArith{P.k64}, stream);
-}
-
-template <typename T>
-int launch_sized(const Params& P, bool precise, hipStream_t stream) {
-  if (P.num_nodes <= kCapSmall) return launch_cap<T, kCapSmall, kSlotsSmall>(P, precise, stream);
-  if (P.num_nodes <= kCapMid) return launch_cap<T, kCapMid, kSlotsMid>(P, precise, stream);
-  return launch_cap<T, kCapLarge, kSlotsLarge>(P, precise, stream);
+  return launch_typed<T, PreciseArith, kCap>(P, PreciseArith{P.k64}, stream);
 }
 
 }  // namespace
@@ -1791,8 +1685,12 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   P.k64 = 1.4426950408889634 / static_cast<double>(a.temperature);
   P.k32 = static_cast<float>(P.k64);
   const bool precise = a.dtype == TV_DTYPE_F32 || a.vocab < kPreciseBelowVocab;
-  if (a.dtype == TV_DTYPE_BF16) return launch_sized<uint16_t>(P, precise, stream);
-  return launch_sized<float>(P, true, stream);
+  const bool small = a.num_nodes <= kCapSmall;
+  if (a.dtype == TV_DTYPE_BF16)
+    return small ? launch_cap<uint16_t, kCapSmall>(P, precise, stream)
+                 : launch_cap<uint16_t, kCapLarge>(P, precise, stream);
+  return small ? launch_cap<float, kCapSmall>(P, true, stream)
+               : launch_cap<float, kCapLarge>(P, true, stream);
 }
 
 }  // namespace tv

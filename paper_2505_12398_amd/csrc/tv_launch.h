@@ -36,15 +36,12 @@ struct VerifyArgs {
 constexpr int kMaxGrid = 4096;        // workgroups of one launch
 constexpr int kMaxGroup = 64;         // workgroups that verify one tree together
 constexpr int kMaxBatchPasses = 8;    // passes computed together for one tree
-constexpr int kMaxSlots = 4;          // trees a group verifies at once
-constexpr int kMaxGroupPasses = kMaxSlots * kMaxBatchPasses;
 constexpr int kSegPartBytes = 32;     // one member's partial result of one pass
 constexpr int kCounterStride = 128;   // bytes between the groups' counters
 
 // Device workspace: a header (the abort flag), one counter per group, and the
-// members' partial results of every pass of a group batch, double buffered by
-// batch parity. Groups times members never exceed kMaxGrid, nor batch times
-// kMaxGroup.
+// members' partial results, double buffered by batch parity. Groups times
+// members never exceed kMaxGrid, nor batch times kMaxGroup.
 struct WorkspaceLayout {
   size_t off_counters;     // uint32_t counters, kCounterStride bytes apart
   size_t off_parts;        // partials [group][parity][pass][member]
@@ -63,7 +60,7 @@ inline WorkspaceLayout workspace_layout(int32_t batch, int32_t vocab) {
   L.off_counters = off;
   off = align256(off + static_cast<size_t>(kCounterStride) * (groups < 1 ? 1 : groups));
   L.off_parts = off;
-  off = align256(off + static_cast<size_t>(kSegPartBytes) * 2 * kMaxGroupPasses *
+  off = align256(off + static_cast<size_t>(kSegPartBytes) * 2 * kMaxBatchPasses *
                            (wg < 1 ? 1 : wg));
   L.bytes = off;
   return L;
