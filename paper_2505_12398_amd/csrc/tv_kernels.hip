@@ -266,7 +266,11 @@ struct WgScratch {
   int hit;                  // first thread whose range holds the sample
   int last_pos;             // last thread with positive weight
   int smp_seg;
-  double smp_target;        // mass still to cover inside the chosen stripe
+  int smp_chunk;            // chunk of the stripe holding the sample (-1: none yet)
+  int smp_last_chunk;       // last chunk with positive mass
+  double smp_target;        // mass still to cover inside the chosen stripe / chunk
+  double smp_window;        // mass of the window of chunks just scanned
+  double smp_chunks[256];   // chunk sums of one window
 };
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -1295,12 +1299,19 @@ __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
 
 // Inverse-CDF draw of Y (all threads of one member). The weights of the
 // stripes come from the partials of pass 0 of the batch just completed; the
-// stripe holding u*W is rescanned.
+// stripe holding u*W is rescanned. Its units (head elements, 16-byte vectors,
+// tail elements, in token order) are summed in chunks of 64 consecutive units,
+// one unit per lane, with many chunks' loads in flight per wave; a scan over
+// the chunk sums finds the chunk, a wave scan over its units the unit, and the
+// lane holding that unit finds the token.
+constexpr int kSampleChunks = 256;      // chunk sums held at once (a window)
+constexpr int kSampleInFlight = 2;      // chunks per wave whose loads are in flight
+
 template <typename T, class A, int kCap>
 __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
                                                        const Lds<Params>& P, A ar, int g) {
   constexpr int E = Elem<T>::E;
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int node = sm.bnode[0];
   const int G = P.G;
   if (tid < 64) {
@@ -1336,18 +1347,17 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
         fallback = true;
       }
     }
-    if (lane == 0) ws.smp_seg = seg;
+    if (lane == 0) {
+      ws.smp_seg = seg;
+      ws.smp_chunk = -1;
+      ws.smp_last_chunk = -1;
+    }
     if (seg >= 0 && lane == seg) ws.smp_target = fallback ? INFINITY : target - (incl - w);
   }
-  if (tid == 0) {
-    ws.hit = kNT;
-    ws.last_pos = -1;
-    sm.res_y = -2;
-  }
+  if (tid == 0) sm.res_y = -2;
   __syncthreads();
   const int seg = ws.smp_seg;
   if (seg < 0) return;     // no mass: res_y stays negative (degenerate)
-  const double local = ws.smp_target;
   const T* rb = row_ptr<T>(P, P.target, sm.tree, node);
   const T* rs = row_ptr<T>(P, P.draft, sm.tree, node);
   const Geom geo = row_geom(rb, P.vocab);
@@ -1356,89 +1366,168 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
   const int nv = max(0, r.ve - r.vb);
   const int nt = r.last ? geo.tail : 0;
   const int nu = nh + nv + nt;
-  const int u0 = static_cast<int>((static_cast<long long>(tid) * nu) / kNT);
-  const int u1 = static_cast<int>((static_cast<long long>(tid + 1) * nu) / kNT);
-  const TermParams tp{sm.smp_cb, sm.smp_cs, sm.smp_ap, sm.smp_bp};
   const int tail0 = geo.head + geo.nvec * E;
+  const TermParams tp{sm.smp_cb, sm.smp_cs, sm.smp_ap, sm.smp_bp};
   auto run = [&](auto two_tag) {
     constexpr bool TWO = decltype(two_tag)::value;
     using TM = Terms<A, TWO, false>;
     const TM tm(ar, tp);
     double unused = 0.0;
-    // element weights of unit i of the stripe (a head/tail element or a
-    // vector); returns the count and the first token id
-    auto unit = [&](int i, double (&wd)[E], int& tok0) -> int {
-      if (i < nh || i >= nh + nv) {
-        const int x = i < nh ? i : tail0 + (i - nh - nv);
-        wd[0] = scalar_weight<T, TM, TWO>(tm, rb, rs, x, unused);
-        tok0 = x;
-        return 1;
-      }
-      const int v = r.vb + (i - nh);
-      float xb[E], xs[E];
-      Elem<T>::unpack(load16(rb, geo.head, v), xb);
-      if constexpr (TWO) {
-        Elem<T>::unpack(load16(rs, geo.head, v), xs);
-      } else {
-#pragma unroll
-        for (int e = 0; e < E; ++e) xs[e] = 0.0f;
-      }
-      typename TM::W w[E];
-      tm.weights(xb, xs, w, unused);
-#pragma unroll
-      for (int e = 0; e < E; ++e) wd[e] = static_cast<double>(w[e]);
-      tok0 = geo.head + v * E;
-      return E;
+    // loads of unit i, unconditional: vectors clamped into the stripe (a
+    // stripe without vectors reads a dummy vector of the workspace); head /
+    // tail units are single elements read in unit_sum itself
+    const bool has_vec = nv > 0;
+    const T* lrb = has_vec ? rb : reinterpret_cast<const T*>(P.ws);
+    const T* lrs = has_vec ? rs : reinterpret_cast<const T*>(P.ws);
+    const int lhead = has_vec ? geo.head : 0;
+    const int lvb = has_vec ? r.vb : 0, lvl = has_vec ? r.ve - 1 : 0;
+    auto load_unit = [&](int i, uint4& vb, uint4& vs) {
+      const int v = min(max(lvb + (i - nh), lvb), lvl);
+      vb = load16(lrb, lhead, v);
+      vs = TWO ? load16(lrs, lhead, v) : make_uint4(0, 0, 0, 0);
     };
-    // the same unit sums as the pass: fp32 (fast) or fp64 (precise) per unit
-    auto unit_sum = [&](int i) -> double {
+    // sum of unit i: the same value wherever it is computed
+    auto unit_sum = [&](int i, const uint4& vb, const uint4& vs) -> double {
+      if (i >= nu) return 0.0;
       if (i < nh || i >= nh + nv) {
         const int x = i < nh ? i : tail0 + (i - nh - nv);
         return scalar_weight<T, TM, TWO>(tm, rb, rs, x, unused);
       }
-      const int v = r.vb + (i - nh);
-      const uint4 vb = load16(rb, geo.head, v);
-      const uint4 vs = TWO ? load16(rs, geo.head, v) : make_uint4(0, 0, 0, 0);
       return vec_sum<T, TM, TWO>(tm, vb, vs, unused);
     };
-    double mine = 0.0;
-    for (int i = u0; i < u1; ++i) mine += unit_sum(i);
-    const double incl = block_incl_scan(ws, mine);
-    const double excl = incl - mine;
-    if (mine > 0.0) {
-      if (local < incl)
-        __hip_atomic_fetch_min(&ws.hit, tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      __hip_atomic_fetch_max(&ws.last_pos, tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-    __syncthreads();
-    const bool fallback = ws.hit >= kNT;
-    const int chosen = fallback ? ws.last_pos : ws.hit;
-    if (tid == chosen) {
-      double C = excl;
-      int y = -1, last = -1;
-      for (int i = u0; i < u1 && y < 0; ++i) {
-        const double us = unit_sum(i);
-        double wd[E];
-        int tok0 = 0;
-        const int n = unit(i, wd, tok0);
-        if (!fallback && us > 0.0 && local < C + us) {
-          double C2 = C;
-          for (int e = 0; e < n; ++e) {
-            if (wd[e] > 0.0) {
-              last = tok0 + e;
-              if (local < C2 + wd[e]) { y = tok0 + e; break; }
-            }
-            C2 += wd[e];
-          }
-          if (y < 0) y = last;         // rounding inside the unit: its last positive weight
-        } else {
-          for (int e = 0; e < n; ++e)
-            if (wd[e] > 0.0) last = tok0 + e;
+    double running = 0.0;     // mass of the windows before this one
+    double local = ws.smp_target;
+    for (int w0 = 0; w0 < nu; w0 += kSampleChunks * 64) {
+      const int nck = min(kSampleChunks, (nu - w0 + 63) / 64);
+      // chunk sums: wave w takes chunks w, w + 4, ..., kSampleInFlight at a time
+      for (int c0 = wave; c0 < nck; c0 += kNW * kSampleInFlight) {
+        uint4 lb[kSampleInFlight], ls[kSampleInFlight];
+#pragma unroll
+        for (int j = 0; j < kSampleInFlight; ++j)
+          load_unit(w0 + (c0 + j * kNW) * 64 + lane, lb[j], ls[j]);
+#pragma unroll
+        for (int j = 0; j < kSampleInFlight; ++j) {
+          pin(lb[j]);
+          pin(ls[j]);
         }
-        C += us;
+#pragma unroll
+        for (int j = 0; j < kSampleInFlight; ++j) {
+          const int c = c0 + j * kNW;
+          if (c < nck) {
+            const double s = wave_sum(unit_sum(w0 + c * 64 + lane, lb[j], ls[j]));
+            if (lane == 0) ws.smp_chunks[c] = s;
+          }
+        }
       }
-      if (y < 0) y = last;             // rounding at the end: last positive weight
-      sm.res_y = y;
+      __syncthreads();
+      // the chunk holding the target: lane l of wave 0 scans chunks 4l .. 4l + 3
+      if (tid < 64) {
+        double cs[4], tot = 0.0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = 4 * lane + j;
+          cs[j] = c < nck ? ws.smp_chunks[c] : 0.0;
+          tot += cs[j];
+        }
+        double incl = tot;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const double o = __shfl_up(incl, off, 64);
+          if (lane >= off) incl += o;
+        }
+        double before = running + (incl - tot);
+        int hit = -1, lastpos = -1;
+        double hit_target = 0.0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (cs[j] > 0.0) {
+            lastpos = 4 * lane + j;
+            if (hit < 0 && local < before + cs[j]) {
+              hit = 4 * lane + j;
+              hit_target = local - before;
+            }
+          }
+          before += cs[j];
+        }
+        const uint64_t hits = __ballot(hit >= 0);
+        const uint64_t poss = __ballot(lastpos >= 0);
+        if (hits) {
+          const int l = __ffsll(static_cast<long long>(hits)) - 1;
+          if (lane == l) {
+            ws.smp_chunk = w0 / 64 + hit;
+            ws.smp_target = hit_target;
+          }
+        } else if (poss) {
+          const int l = 63 - __clzll(static_cast<long long>(poss));
+          if (lane == l) ws.smp_last_chunk = w0 / 64 + lastpos;
+        }
+        if (lane == 63) ws.smp_window = incl;   // mass of this window
+      }
+      __syncthreads();
+      if (ws.smp_chunk >= 0) break;
+      running += ws.smp_window;
+    }
+    // rounding at the end: the last chunk with mass, and in it the last
+    // positive weight
+    const bool fallback = ws.smp_chunk < 0;
+    const int chunk = fallback ? ws.smp_last_chunk : ws.smp_chunk;
+    if (chunk < 0) return;    // no positive weight: degenerate
+    if (tid < 64) {
+      const int i = chunk * 64 + lane;
+      uint4 vb, vs;
+      load_unit(i, vb, vs);
+      const double us = unit_sum(i, vb, vs);
+      double incl = us;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const double o = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += o;
+      }
+      const double tgt = fallback ? INFINITY : ws.smp_target;
+      const uint64_t hits = __ballot(us > 0.0 && tgt < incl);
+      const uint64_t poss = __ballot(us > 0.0);
+      int pick = -1;
+      bool last_of_unit = fallback;
+      if (hits) {
+        pick = __ffsll(static_cast<long long>(hits)) - 1;
+      } else if (poss) {                    // rounding at the end: last unit with mass
+        pick = 63 - __clzll(static_cast<long long>(poss));
+        last_of_unit = true;
+      }
+      if (pick >= 0 && lane == pick) {
+        double wd[E];
+        int tok0 = 0, n = 1;
+        if (i < nh || i >= nh + nv) {
+          const int x = i < nh ? i : tail0 + (i - nh - nv);
+          wd[0] = scalar_weight<T, TM, TWO>(tm, rb, rs, x, unused);
+          tok0 = x;
+        } else {
+          float xb[E], xs[E];
+          Elem<T>::unpack(vb, xb);
+          if constexpr (TWO) {
+            Elem<T>::unpack(vs, xs);
+          } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e) xs[e] = 0.0f;
+          }
+          typename TM::W wv[E];
+          tm.weights(xb, xs, wv, unused);
+#pragma unroll
+          for (int e = 0; e < E; ++e) wd[e] = static_cast<double>(wv[e]);
+          tok0 = geo.head + (r.vb + (i - nh)) * E;
+          n = E;
+        }
+        double C = incl - us;
+        int y = -1, last = -1;
+        for (int e = 0; e < n; ++e) {
+          if (wd[e] > 0.0) {
+            last = tok0 + e;
+            if (!last_of_unit && y < 0 && tgt < C + wd[e]) y = tok0 + e;
+          }
+          C += wd[e];
+        }
+        sm.res_y = y >= 0 ? y : last;    // rounding inside the unit: its last positive weight
+      }
     }
   };
   if (sm.smp_two) run(std::true_type{});
