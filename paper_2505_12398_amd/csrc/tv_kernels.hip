@@ -57,6 +57,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "tv.h"
@@ -1699,14 +1700,37 @@ constexpr int kPreciseBelowVocab = 16384;
 
 template <typename T, class A, int kCap>
 int launch_typed(Params P, A ar, hipStream_t stream) {
-  int dev = 0, cus = 0, clock_khz = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return TV_ERR_HIP;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
-    return TV_ERR_HIP;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, verify_kernel<T, A, kCap>, kNT, 0) !=
-      hipSuccess)
-    return TV_ERR_HIP;
+  // device properties and the kernel's occupancy, queried once per device
+  struct DevInfo {
+    int cus, clock_khz, per_cu;
+  };
+  constexpr int kMaxDevices = 64;
+  static DevInfo info[kMaxDevices];
+  static bool have[kMaxDevices];
+  static std::mutex mu;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TV_ERR_HIP;
+  DevInfo di{};
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (dev < kMaxDevices && have[dev]) {
+      di = info[dev];
+    } else {
+      if (hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+              hipSuccess ||
+          hipDeviceGetAttribute(&di.clock_khz, hipDeviceAttributeWallClockRate, dev) !=
+              hipSuccess ||
+          hipOccupancyMaxActiveBlocksPerMultiprocessor(&di.per_cu, verify_kernel<T, A, kCap>, kNT,
+                                                       0) != hipSuccess)
+        return TV_ERR_HIP;
+      if (dev < kMaxDevices) {
+        info[dev] = di;
+        have[dev] = true;
+      }
+    }
+  }
+  const int cus = di.cus, clock_khz = di.clock_khz;
+  int per_cu = di.per_cu;
   if (per_cu < 1) per_cu = 1;
   long long resident = static_cast<long long>(per_cu) * (cus > 0 ? cus : 1);
   if (resident > tv::kMaxGrid) resident = tv::kMaxGrid;
