@@ -26,20 +26,23 @@
  *
  * Memory and streams. Every pointer is a device pointer. The caller owns all
  * buffers, including a device workspace of tv_workspace_size() bytes that the
- * call uses as scratch (work queue, counters and partial sums; its contents
- * need no initialisation and are meaningless afterwards). The library
+ * call uses as scratch (per-group counters and the partial sums of every
+ * vocabulary pass; its contents need no initialisation and are meaningless
+ * afterwards). The library
  * allocates nothing, keeps no state between calls and never synchronises the
  * host: work is enqueued on `stream` and the call returns. Inputs are
  * read-only. Outputs are written for every tree, including trees whose status
  * is not TV_TREE_OK (they get -1 sentinels). Calls that write the same output
  * buffers or share a workspace must be ordered by the caller.
  *
- * Execution. One call launches a persistent grid of at most as many
- * workgroups as the device can hold at once; idle workgroups wait for work in
- * the other trees of the batch. Calls on concurrent streams of one device can
- * therefore hold each other's workgroups back; every wait is bounded, and a
- * call that makes no progress for 4 seconds gives up and reports
- * TV_TREE_ABORTED for the trees it did not finish.
+ * Execution. One call makes one cooperative launch of at most as many
+ * workgroups as the device holds at once, in groups that each verify one tree
+ * at a time (several workgroups per tree when the batch is small). The
+ * members of a group exchange partial sums through the workspace and wait for
+ * each other at every vocabulary pass; the launch waits until the whole grid
+ * can be resident. Every wait inside the kernel is bounded: a call that makes
+ * no progress for 4 seconds gives up and reports TV_TREE_ABORTED for the
+ * trees it did not finish.
  *
  * Errors. Argument problems the host can see (null pointers, sizes, enums,
  * temperature, misaligned pointers) return a tv_status_t other than TV_OK and
@@ -125,8 +128,8 @@ enum {
 
 /*
  * Bytes of device workspace tv_verify / tv_verify_tokenlevel need for these
- * sizes (valid for either dtype; at most about 65 MiB, about 16 MiB for 256
- * trees at V = 128256). Returns 0 for invalid sizes (batch < 1, vocab < 2 or
+ * sizes (valid for either dtype; at most about 2.5 MiB, about 2.0 MiB for 256
+ * trees). Returns 0 for invalid sizes (batch < 1, vocab < 2 or
  * beyond the limits below); a batch of 0 needs no workspace.
  */
 size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab);

@@ -75,7 +75,7 @@ def test_workspace_size():
     assert sizes == sorted(sizes)
     assert sizes[-1] == sizes[-2]          # capped by the number of workgroups per call
     assert ws(16, 65, 2) <= ws(16, 65, 128256) <= ws(16, 65, tv.TV_MAX_VOCAB)
-    assert ws(tv.TV_MAX_BATCH, tv.TV_MAX_NODES, tv.TV_MAX_VOCAB) <= 65 << 20
+    assert ws(tv.TV_MAX_BATCH, tv.TV_MAX_NODES, tv.TV_MAX_VOCAB) <= 3 << 20
     # independent of the tree size
     assert ws(256, 2, 128256) == ws(256, tv.TV_MAX_NODES, 128256)
 
