@@ -44,15 +44,17 @@
 // Every sum is formed in a fixed order (per thread, across the workgroup, then
 // across members), so results are reproducible for a given group size.
 //
-// Synchronisation. A member writes its partials with agent-scope atomic stores
-// (written through to the device-coherent level), waits for them to be
-// acknowledged, then increments the group's counter; members wait until the
-// counter reaches G times the batch number, issue an agent-scope acquire fence
-// and read the partials with agent-scope atomic loads. Partials are double
-// buffered by batch parity: a member can only start batch k+2 after every
-// member has finished batch k+1, hence has read batch k. Every wait is bounded
-// by a wall-clock limit after which the launch is abandoned (trees not
-// finished then report TV_TREE_ABORTED), so no wave can spin forever.
+// Synchronisation. A member writes each partial as four 64-bit words with
+// agent-scope atomic stores; every word carries the batch's tag bit (a spare
+// bit: the sign of a sum, the lowest mantissa bit of a float maximum widened
+// to double). Members poll the G partials of a pass with agent-scope atomic
+// loads until all words carry the expected tag: 64-bit accesses are single-copy
+// atomic, so each word read is whole, and no counter, fence or second round of
+// loads is needed. Partials are double buffered by batch parity and the tag
+// alternates between the uses of a buffer: a member can only write batch k+2
+// after every member has written batch k+1, hence has read batch k. Every wait
+// is bounded by a wall-clock limit after which the launch is abandoned (trees
+// not finished then report TV_TREE_ABORTED), so no wave can spin forever.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -78,7 +80,7 @@ static_assert(kMaxGroup <= 64, "member partials are combined by one wavefront");
 // Pass kinds and controller commands.
 enum : int {
   kCmdNone = 0, kCmdStats2 = 1, kCmdStats1 = 2, kCmdSPass = 3, kCmdSPassSd = 4, kCmdWSum = 5,
-  kCmdLocalSample = 6, kCmdDone = 7, kCmdBatch = 8
+  kCmdLocalSample = 6, kCmdDone = 7, kCmdBatch = 8, kCmdAbandon = 9
 };
 enum : int {
   kPhDescend = 0, kPhTest, kPhAfterSPass, kPhFinal, kPhFinalLeafStats, kPhFinalWSum,
@@ -104,7 +106,7 @@ struct Params {
   float* p_init;
   int32_t* counters;
   uint8_t* ws;
-  size_t off_counters, off_parts;
+  size_t off_parts, parts_words;
   long long spin_limit;      // wall-clock ticks a wait may last before the launch is abandoned
   int batch;
   int num_nodes;
@@ -126,10 +128,41 @@ __device__ __forceinline__ Lds<X>& lds_ref(X& x) {
   return *reinterpret_cast<Lds<X>*>((__attribute__((address_space(3))) void*)&x);
 }
 
-struct SegPart {             // 32 bytes: one member's partial result of one pass
+// One member's partial result of one pass: four 64-bit words (two sums, two
+// maxima), each written and read with a single-copy atomic 64-bit access and
+// each carrying the batch's tag bit, so a reader that sees the expected tag in
+// all four words has the whole result of that batch. The sums are >= 0 (or
+// NaN) and carry the tag in the sign bit; the maxima are floats widened to
+// doubles, whose lowest mantissa bit is always 0, and carry it there.
+struct SegPart {
+  uint64_t w[4];
+};
+
+// Tag bit of batch `seq` (1, 2, ...): the two parity buffers are used by
+// batches 1, 3, 5, ... and 2, 4, 6, ...; the tag alternates between the uses
+// of a buffer, starting at 1 (buffers are cleared to 0 before each launch).
+__device__ __forceinline__ uint64_t batch_tag(uint32_t seq) { return ((seq + 1u) >> 1) & 1u; }
+
+__device__ __forceinline__ uint64_t enc_sum(double v, uint64_t tag) {
+  return (static_cast<uint64_t>(__double_as_longlong(v)) & ~(1ull << 63)) | (tag << 63);
+}
+__device__ __forceinline__ double dec_sum(uint64_t w) {
+  return __longlong_as_double(static_cast<long long>(w & ~(1ull << 63)));
+}
+__device__ __forceinline__ uint64_t enc_max(float v, uint64_t tag) {
+  return static_cast<uint64_t>(__double_as_longlong(static_cast<double>(v))) | tag;
+}
+__device__ __forceinline__ float dec_max(uint64_t w) {
+  return static_cast<float>(__longlong_as_double(static_cast<long long>(w & ~1ull)));
+}
+__device__ __forceinline__ bool tags_are(const uint64_t (&w)[4], uint64_t tag) {
+  return (w[0] >> 63) == tag && (w[1] >> 63) == tag && (w[2] & 1u) == tag && (w[3] & 1u) == tag;
+}
+
+// The sums and maxima a stripe pass produces.
+struct StripeResult {
   double s0, s1;
   float m0, m1;
-  uint32_t pad[2];
 };
 
 // ---------------------------------------------------------------------------
@@ -139,11 +172,6 @@ struct SegPart {             // 32 bytes: one member's partial result of one pas
 template <class PP>
 __device__ __forceinline__ uint32_t* ws_abort(const PP& P) {
   return reinterpret_cast<uint32_t*>(P.ws);
-}
-template <class PP>
-__device__ __forceinline__ uint32_t* ws_counter(const PP& P, int g) {
-  return reinterpret_cast<uint32_t*>(P.ws + P.off_counters + static_cast<size_t>(g) *
-                                                                 tv::kCounterStride);
 }
 // partial of member m for pass p of the batch with parity `par` in group g
 template <class PP>
@@ -163,22 +191,6 @@ __device__ __forceinline__ void st_rlx(uint64_t* p, uint64_t v) {
 }
 __device__ __forceinline__ void st_rlx(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ double ld_rlx_f64(const double* p) {
-  return __longlong_as_double(static_cast<long long>(
-      ld_rlx(reinterpret_cast<const uint64_t*>(p))));
-}
-__device__ __forceinline__ void st_rlx_f64(double* p, double v) {
-  st_rlx(reinterpret_cast<uint64_t*>(p), static_cast<uint64_t>(__double_as_longlong(v)));
-}
-__device__ __forceinline__ void fence_acquire() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
-// Waits until this thread's earlier stores are acknowledged (s_waitcnt
-// vmcnt(0)); with the stores made through st_rlx this orders them before a
-// later signalling atomic. The signal fence keeps the compiler from moving
-// memory operations across it.
-__device__ __forceinline__ void stores_done() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // ---------------------------------------------------------------------------
@@ -578,7 +590,7 @@ __device__ __forceinline__ void stream_stripe(const T* rb, const T* rs, int head
 
 template <typename T, class A, bool TWO>
 __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
-                             const SegRange& r, const A& ar, SegPart& out) {
+                             const SegRange& r, const A& ar, StripeResult& out) {
   constexpr int E = Elem<T>::E;
   const int tid = threadIdx.x;
   Online ob = online_init(ar), os = online_init(ar);
@@ -624,7 +636,8 @@ __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const
 
 template <typename T, class A, bool SD>
 __device__ void stripe_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
-                            const SegRange& r, const A& ar, const TermParams& p, SegPart& out) {
+                            const SegRange& r, const A& ar, const TermParams& p,
+                            StripeResult& out) {
   const Terms<A, true, SD> tm(ar, p);
   using TM = Terms<A, true, SD>;
   const int tid = threadIdx.x;
@@ -1223,29 +1236,68 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
 // Group exchange: combining the members' partials, the local sample
 // ---------------------------------------------------------------------------
 
+// Loads member `lane`'s partial of one pass until all four words carry the
+// batch's tag (all lanes < G of the wave). Returns false if the launch was
+// abandoned meanwhile (the wait limit passed here or elsewhere).
+template <class PP>
+__device__ __forceinline__ bool await_part(const PP& P, const SegPart* part, int G,
+                                           uint64_t tag, uint64_t (&w)[4]) {
+  const int lane = threadIdx.x & 63;
+  const long long t0 = wall_clock64();
+  for (int it = 0;; ++it) {
+    bool ok = true;
+    if (lane < G) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = ld_rlx(&part[lane].w[j]);
+      ok = tags_are(w, tag);
+    }
+    if (__ballot(!ok) == 0) return true;
+    __builtin_amdgcn_s_sleep(1);
+    if ((it & 15) == 15) {
+      uint32_t ab = 0;
+      if (lane == 0) ab = ld_rlx(ws_abort(P));
+      if (__shfl(ab, 0, 64)) return false;
+      if (wall_clock64() - t0 > P.spin_limit) {
+        if (lane == 0) st_rlx(ws_abort(P), 1u);
+        return false;
+      }
+    }
+  }
+}
+
 // Combines the members' partials of the completed batch (all threads): wave w
-// takes passes w, w + 4, lanes are members; STATS results go to the node
-// arrays, a SPASS / WSUM result to res_S / res_sd.
+// waits for and takes passes w, w + 4, lanes are members; STATS results go to
+// the node arrays, a SPASS / WSUM result to res_S / res_sd. Returns false if
+// the launch was abandoned.
 template <typename T, class A, int kCap>
-__device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
+__device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
+                                                       Lds<WgScratch>& ws,
                                                        const Lds<Params>& P, A ar, int g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bn = sm.bn;
   const int G = P.G;
   const int par = static_cast<int>(sm.seq & 1u);
-  fence_acquire();
+  const uint64_t tag = batch_tag(sm.seq);
+  if (tid == 0) ws.stop = 0;
+  __syncthreads();
+  // no line of the partials cached from an earlier batch is used
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   for (int p = wave; p < bn; p += kNW) {
     const int cmd = sm.bcmd[p];
     const int node = sm.bnode[p];
     const SegPart* part = ws_parts(P, g, par, p);
+    uint64_t w[4] = {0, 0, 0, 0};
+    if (!await_part(P, part, G, tag, w)) {
+      if (lane == 0) ws.stop = 1;
+      break;
+    }
     double s0 = 0.0, s1 = 0.0;
     float m0 = -INFINITY, m1 = -INFINITY;
     if (lane < G) {
-      s0 = ld_rlx_f64(&part[lane].s0);
-      s1 = ld_rlx_f64(&part[lane].s1);
-      const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
-      m0 = __uint_as_float(static_cast<uint32_t>(mm));
-      m1 = __uint_as_float(static_cast<uint32_t>(mm >> 32));
+      s0 = dec_sum(w[0]);
+      s1 = dec_sum(w[1]);
+      m0 = dec_max(w[2]);
+      m1 = dec_max(w[3]);
     }
     if (cmd == kCmdStats2 || cmd == kCmdStats1) {
       const bool two = cmd == kCmdStats2;
@@ -1279,6 +1331,7 @@ __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
     }
   }
   __syncthreads();
+  if (ws.stop) return false;
   // children's original ratios r0 = p(x)/q(x) and draft terms
   const double kd = ar.kd();
   for (int p = 0; p < bn; ++p) {
@@ -1296,6 +1349,7 @@ __device__ __attribute__((always_inline)) void combine(Lds<TreeSmem<kCap>>& sm,
     }
   }
   __syncthreads();
+  return true;
 }
 
 // Inverse-CDF draw of Y (all threads of one member). The weights of the
@@ -1319,10 +1373,10 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
     const SegPart* part = ws_parts(P, g, static_cast<int>(sm.seq & 1u), 0);
     double w = 0.0;
     if (lane < G) {
-      const double s0 = ld_rlx_f64(&part[lane].s0);
+      // the combine has seen this batch's tags in every word
+      const double s0 = dec_sum(ld_rlx(&part[lane].w[0]));
       if (sm.smp_from_stats) {
-        const uint64_t mm = ld_rlx(reinterpret_cast<const uint64_t*>(&part[lane].m0));
-        const float m0 = __uint_as_float(static_cast<uint32_t>(mm));
+        const float m0 = dec_max(ld_rlx(&part[lane].w[2]));
         w = (m0 > -INFINITY) ? s0 * exp2(sm.smp_cb - ar.frame(m0)) : 0.0;
       } else {
         w = s0;
@@ -1548,7 +1602,11 @@ __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& s
   if (sm.status == TV_TREE_OK) {
     int done_cmd = kCmdNone;
     if (sm.pending) {
-      combine<T, A>(sm, P, ar, g);
+      if (!combine<T, A>(sm, ws, P, ar, g)) {   // the launch was abandoned
+        if (tid == 0) sm.cmd = kCmdAbandon;
+        __syncthreads();
+        return;
+      }
       done_cmd = sm.bcmd[0];
       if (tid == 0) sm.pending = 0;
     }
@@ -1572,14 +1630,16 @@ __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& s
 }
 
 // This member's share of the batch in sm.b* (all threads): its stripe of every
-// pass, then the group exchange. Returns false if the launch was abandoned.
+// pass, published as tagged partials. The members' partials are awaited in the
+// next controller step.
 template <typename T, class A, int kCap>
-__device__ __forceinline__ bool run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
+__device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
                                           const Params& P, const A& ar, int g, int m) {
   const int tid = threadIdx.x;
   const int bn = sm.bn;
   const uint32_t seq = sm.seq + 1u;
   const int par = static_cast<int>(seq & 1u);
+  const uint64_t tag = batch_tag(seq);
   const int b = sm.tree;
   for (int p = 0; p < bn; ++p) {
     const int node = sm.bnode[p];
@@ -1588,7 +1648,7 @@ __device__ __forceinline__ bool run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     const T* rs = row_ptr<T>(P, P.draft, b, node);
     const Geom geo = row_geom(rb, P.vocab);
     const SegRange r = stripe(geo, m, P.G);
-    SegPart part;
+    StripeResult part;
     switch (cmd) {
       case kCmdStats2: stripe_stats<T, A, true>(ws, rb, rs, geo, r, ar, part); break;
       case kCmdStats1: stripe_stats<T, A, false>(ws, rb, rs, geo, r, ar, part); break;
@@ -1601,15 +1661,26 @@ __device__ __forceinline__ bool run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     }
     if (tid == 0) {
       SegPart* dst = ws_parts(P, g, par, p) + m;
-      st_rlx_f64(&dst->s0, part.s0);
-      st_rlx_f64(&dst->s1, part.s1);
-      st_rlx(reinterpret_cast<uint64_t*>(&dst->m0),
-             (static_cast<uint64_t>(__float_as_uint(part.m1)) << 32) | __float_as_uint(part.m0));
+      st_rlx(&dst->w[0], enc_sum(part.s0, tag));
+      st_rlx(&dst->w[1], enc_sum(part.s1, tag));
+      st_rlx(&dst->w[2], enc_max(part.m0, tag));
+      st_rlx(&dst->w[3], enc_max(part.m1, tag));
     }
   }
   if (tid == 0) {
-    stores_done();
-    __hip_atomic_fetch_add(ws_counter(P, g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // The entries of the passes this batch does not have are written too, so
+    // that every entry of a parity buffer is rewritten at each use and its tag
+    // alternates: an entry left from two uses earlier would carry the tag the
+    // next reader expects.
+    for (int p = bn; p < kMaxBatch; ++p) {
+      SegPart* dst = ws_parts(P, g, par, p) + m;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) st_rlx(&dst->w[j], j < 2 ? enc_sum(0.0, tag) : enc_max(0.0f, tag));
+    }
+    // This batch's stores are performed before any store of the next batch is
+    // issued, so a member that has seen this member's next partials will find
+    // these, not the ones from two uses earlier, which carry the same tag.
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     sm.seq = seq;
     sm.pending = 1;
     // the weights of pass 0 stay available for drawing Y at its node
@@ -1620,42 +1691,21 @@ __device__ __forceinline__ bool run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     sm.last_cb = sm.cmd_cb;
     sm.last_cs = sm.cmd_cs;
   }
-  // wait for the other members' partials
-  if (tid < 64) {
-    const uint32_t want = seq * static_cast<uint32_t>(P.G);
-    const long long t0 = wall_clock64();
-    int stop = 0;
-    for (int it = 0;; ++it) {
-      uint32_t c = 0;
-      if (tid == 0) c = ld_rlx(ws_counter(P, g));
-      c = __shfl(c, 0, 64);
-      if (static_cast<int32_t>(c - want) >= 0) break;
-      if ((it & 15) == 15) {
-        uint32_t ab = 0;
-        if (tid == 0) ab = ld_rlx(ws_abort(P));
-        ab = __shfl(ab, 0, 64);
-        if (ab) { stop = 1; break; }
-        if (wall_clock64() - t0 > P.spin_limit) {
-          if (tid == 0) st_rlx(ws_abort(P), 1u);
-          stop = 1;
-          break;
-        }
-      }
-    }
-    if (tid == 0) ws.stop = stop;
-  }
   __syncthreads();
-  return !ws.stop;
 }
 
 // ---------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------
 
+// Clears the abort flag and the partials (tag 0: no batch yet) and marks every
+// tree aborted until it is finished.
 __global__ void __launch_bounds__(256) init_kernel(Params P) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i == 0) *ws_abort(P) = 0u;
-  if (i < P.ngroups) *ws_counter(P, i) = 0u;
+  uint64_t* parts = reinterpret_cast<uint64_t*>(P.ws + P.off_parts);
+  for (size_t k = i; k < P.parts_words; k += static_cast<size_t>(gridDim.x) * blockDim.x)
+    parts[k] = 0u;
   if (i < P.batch) {
     P.status[i] = TV_TREE_ABORTED;
     P.accept_len[i] = -1;
@@ -1687,7 +1737,11 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
     for (;;) {
       controller_step<T, A>(sm, ws, Ps, ar, g, m);
       if (sm.cmd == kCmdDone) break;
-      if (!(live = run_batch<T, A>(sm, ws, P, ar, g, m))) break;
+      if (sm.cmd == kCmdAbandon) {
+        live = false;
+        break;
+      }
+      run_batch<T, A>(sm, ws, P, ar, g, m);
     }
     if (!live) break;
     if (m == 0) finish_tree(sm, Ps);
@@ -1746,9 +1800,12 @@ int launch_typed(Params P, A ar, hipStream_t stream) {
   P.G = static_cast<int>(G);
   P.ngroups = static_cast<int>(ngroups);
   P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s
-  const long long init_n = P.batch > ngroups ? P.batch : ngroups;
-  hipLaunchKernelGGL(init_kernel, dim3(static_cast<unsigned>((init_n + 255) / 256)), dim3(256), 0,
-                     stream, P);
+  long long init_n = static_cast<long long>(P.parts_words);
+  if (init_n < P.batch) init_n = P.batch;
+  long long init_blocks = (init_n + 255) / 256;
+  if (init_blocks > 1024) init_blocks = 1024;     // the partials are cleared in a grid-stride loop
+  hipLaunchKernelGGL(init_kernel, dim3(static_cast<unsigned>(init_blocks)), dim3(256), 0, stream,
+                     P);
   if (hipGetLastError() != hipSuccess) return TV_ERR_HIP;
   // cooperative: the members of a group wait for each other, so all of them
   // must be resident at once
@@ -1788,8 +1845,8 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   P.p_init = a.p_init;
   P.counters = a.counters;
   P.ws = static_cast<uint8_t*>(workspace);
-  P.off_counters = L.off_counters;
   P.off_parts = L.off_parts;
+  P.parts_words = L.parts_bytes / 8;
   P.batch = a.batch;
   P.num_nodes = a.num_nodes;
   P.vocab = a.vocab;

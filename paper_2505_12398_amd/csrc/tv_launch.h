@@ -37,14 +37,13 @@ constexpr int kMaxGrid = 4096;        // workgroups of one launch
 constexpr int kMaxGroup = 64;         // workgroups that verify one tree together
 constexpr int kMaxBatchPasses = 8;    // passes computed together for one tree
 constexpr int kSegPartBytes = 32;     // one member's partial result of one pass
-constexpr int kCounterStride = 128;   // bytes between the groups' counters
 
-// Device workspace: a header (the abort flag), one counter per group, and the
-// members' partial results, double buffered by batch parity. Groups times
-// members never exceed kMaxGrid, nor batch times kMaxGroup.
+// Device workspace: a header (the abort flag) and the members' partial
+// results, double buffered by batch parity. Groups times members never exceed
+// kMaxGrid, nor batch times kMaxGroup.
 struct WorkspaceLayout {
-  size_t off_counters;     // uint32_t counters, kCounterStride bytes apart
   size_t off_parts;        // partials [group][parity][pass][member]
+  size_t parts_bytes;
   size_t bytes;
 };
 
@@ -53,15 +52,12 @@ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255);
 inline WorkspaceLayout workspace_layout(int32_t batch, int32_t vocab) {
   (void)vocab;
   WorkspaceLayout L{};
-  const int64_t groups = batch < kMaxGrid ? batch : kMaxGrid;
   const int64_t wg = static_cast<int64_t>(batch) * kMaxGroup < kMaxGrid
                          ? static_cast<int64_t>(batch) * kMaxGroup : kMaxGrid;
   size_t off = 256;                                    // header
-  L.off_counters = off;
-  off = align256(off + static_cast<size_t>(kCounterStride) * (groups < 1 ? 1 : groups));
   L.off_parts = off;
-  off = align256(off + static_cast<size_t>(kSegPartBytes) * 2 * kMaxBatchPasses *
-                           (wg < 1 ? 1 : wg));
+  L.parts_bytes = static_cast<size_t>(kSegPartBytes) * 2 * kMaxBatchPasses * (wg < 1 ? 1 : wg);
+  off = align256(off + L.parts_bytes);
   L.bytes = off;
   return L;
 }
