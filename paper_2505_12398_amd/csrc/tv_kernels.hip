@@ -9,9 +9,13 @@
 // quantities, each member computes its fixed 1/G stripe of the rows involved,
 // publishes the stripe's partial results and waits for the other members';
 // every member then combines the G partials in member order and continues.
-// The group only exchanges these partials: one atomic counter per group and a
-// few words per member and pass. The launch is cooperative, so all members of
-// a group are resident together.
+// The group only exchanges these partials, a few words per member and pass.
+// The launch is cooperative, so all members of a group are resident together.
+// A group with no tree left lends its workgroups to running groups as
+// helpers: a helper takes stripes of another group's passes (the group's
+// member 0 publishes each batch for them), so the trees that run longest get
+// more workgroups as the others finish. With helpers the number of stripes
+// of a pass depends on timing, and so do the last bits of the sums.
 //
 // Pass kinds:
 //   STATS   per row: maximum and sum of 2^(z*k - max*k), k = log2(e)/T, over
@@ -107,6 +111,7 @@ struct Params {
   int32_t* counters;
   uint8_t* ws;
   size_t off_parts, parts_words;
+  size_t off_desc, desc_words;
   long long spin_limit;      // wall-clock ticks a wait may last before the launch is abandoned
   int batch;
   int num_nodes;
@@ -114,6 +119,7 @@ struct Params {
   int mode;
   int algo;
   int G;                     // workgroups per group (per tree)
+  int Gx;                    // most contributors (members + helpers) a group's pass has
   int ngroups;               // groups; group g verifies trees g, g + ngroups, ...
   float k32;                 // log2(e) / T rounded to fp32 (fast element path)
   double k64;                // log2(e) / T (precise element path)
@@ -128,12 +134,15 @@ __device__ __forceinline__ Lds<X>& lds_ref(X& x) {
   return *reinterpret_cast<Lds<X>*>((__attribute__((address_space(3))) void*)&x);
 }
 
-// One member's partial result of one pass: four 64-bit words (two sums, two
-// maxima), each written and read with a single-copy atomic 64-bit access and
-// each carrying the batch's tag bit, so a reader that sees the expected tag in
-// all four words has the whole result of that batch. The sums are >= 0 (or
-// NaN) and carry the tag in the sign bit; the maxima are floats widened to
-// doubles, whose lowest mantissa bit is always 0, and carry it there.
+// One contributor's partial result of one pass: four 64-bit words (two sums,
+// two maxima), each written and read with a single-copy atomic 64-bit access
+// and each carrying a 'written' bit and the batch's tag bit, so a reader that
+// sees both in all four words has the whole result of that batch. The sums
+// are >= 0 (or NaN): the tag is their sign bit and the written bit their last
+// mantissa bit (the sum loses that bit). The maxima are floats widened to
+// doubles, whose low 29 mantissa bits are 0: bit 0 is the written bit, bit 1
+// the tag, bits 2-7 carry a small count (member 0 reports the number of
+// helpers for the next batch in the draft maximum of pass 0).
 struct SegPart {
   uint64_t w[4];
 };
@@ -143,20 +152,25 @@ struct SegPart {
 // of a buffer, starting at 1 (buffers are cleared to 0 before each launch).
 __device__ __forceinline__ uint64_t batch_tag(uint32_t seq) { return ((seq + 1u) >> 1) & 1u; }
 
+constexpr uint64_t kSumMeta = (1ull << 63) | 1ull;
 __device__ __forceinline__ uint64_t enc_sum(double v, uint64_t tag) {
-  return (static_cast<uint64_t>(__double_as_longlong(v)) & ~(1ull << 63)) | (tag << 63);
+  return (static_cast<uint64_t>(__double_as_longlong(v)) & ~kSumMeta) | (tag << 63) | 1ull;
 }
 __device__ __forceinline__ double dec_sum(uint64_t w) {
-  return __longlong_as_double(static_cast<long long>(w & ~(1ull << 63)));
+  return __longlong_as_double(static_cast<long long>(w & ~kSumMeta));
 }
-__device__ __forceinline__ uint64_t enc_max(float v, uint64_t tag) {
-  return static_cast<uint64_t>(__double_as_longlong(static_cast<double>(v))) | tag;
+__device__ __forceinline__ uint64_t enc_max(float v, uint64_t tag, uint64_t count = 0) {
+  return static_cast<uint64_t>(__double_as_longlong(static_cast<double>(v))) | 1ull | (tag << 1) |
+         (count << 2);
 }
 __device__ __forceinline__ float dec_max(uint64_t w) {
-  return static_cast<float>(__longlong_as_double(static_cast<long long>(w & ~1ull)));
+  return static_cast<float>(__longlong_as_double(static_cast<long long>(w & ~0xFFull)));
 }
+__device__ __forceinline__ int max_count(uint64_t w) { return static_cast<int>((w >> 2) & 63u); }
 __device__ __forceinline__ bool tags_are(const uint64_t (&w)[4], uint64_t tag) {
-  return (w[0] >> 63) == tag && (w[1] >> 63) == tag && (w[2] & 1u) == tag && (w[3] & 1u) == tag;
+  const uint64_t mm = 1ull | (tag << 1);
+  return (w[0] & kSumMeta) == ((tag << 63) | 1ull) && (w[1] & kSumMeta) == ((tag << 63) | 1ull) &&
+         (w[2] & 3u) == mm && (w[3] & 3u) == mm;
 }
 
 // The sums and maxima a stripe pass produces.
@@ -177,7 +191,7 @@ __device__ __forceinline__ uint32_t* ws_abort(const PP& P) {
 template <class PP>
 __device__ __forceinline__ SegPart* ws_parts(const PP& P, int g, int par, int p) {
   return reinterpret_cast<SegPart*>(P.ws + P.off_parts) +
-         ((static_cast<size_t>(g) * 2 + par) * kMaxBatch + p) * P.G;
+         ((static_cast<size_t>(g) * 2 + par) * kMaxBatch + p) * P.Gx;
 }
 
 __device__ __forceinline__ uint64_t ld_rlx(const uint64_t* p) {
@@ -284,6 +298,14 @@ struct WgScratch {
   double smp_target;        // mass still to cover inside the chosen stripe / chunk
   double smp_window;        // mass of the window of chunks just scanned
   double smp_chunks[256];   // chunk sums of one window
+  int hnext;                // helpers member 0 reported for the next batch
+  // a helper's view of the group it helps
+  int help_g, help_h, help_state;
+  uint32_t d_seq;
+  int d_tree, d_bn, d_geff;
+  int16_t d_node[8];
+  int8_t d_cmd[8];
+  double d_ap, d_bp, d_cb, d_cs;
 };
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -705,6 +727,8 @@ struct TreeSmem {
   // the batch in flight, then just completed
   int pending;
   uint32_t seq;                    // batches this group has run (all trees so far)
+  int geff;                        // contributors (members + helpers) of the next batch
+  int geff_last;                   // contributors of the batch just completed
   int spass_node;                  // node whose SPASS partials are in the workspace (-1: none)
   double last_ap, last_bp, last_cb, last_cs;
   // local sample request
@@ -1275,7 +1299,7 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
                                                        const Lds<Params>& P, A ar, int g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bn = sm.bn;
-  const int G = P.G;
+  const int G = sm.geff;                // contributors of this batch
   const int par = static_cast<int>(sm.seq & 1u);
   const uint64_t tag = batch_tag(sm.seq);
   if (tid == 0) ws.stop = 0;
@@ -1299,6 +1323,7 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
       m0 = dec_max(w[2]);
       m1 = dec_max(w[3]);
     }
+    if (p == 0 && lane == 0) ws.hnext = max_count(w[3]);   // member 0's report
     if (cmd == kCmdStats2 || cmd == kCmdStats1) {
       const bool two = cmd == kCmdStats2;
       const float Mb = wave_max(m0);
@@ -1332,6 +1357,11 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
   }
   __syncthreads();
   if (ws.stop) return false;
+  if (tid == 0) {
+    sm.geff_last = G;
+    const int next = P.G + ws.hnext;
+    sm.geff = next > G ? next : G;
+  }
   // children's original ratios r0 = p(x)/q(x) and draft terms
   const double kd = ar.kd();
   for (int p = 0; p < bn; ++p) {
@@ -1368,7 +1398,7 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
   constexpr int E = Elem<T>::E;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int node = sm.bnode[0];
-  const int G = P.G;
+  const int G = sm.geff_last;           // contributors of the batch just completed
   if (tid < 64) {
     const SegPart* part = ws_parts(P, g, static_cast<int>(sm.seq & 1u), 0);
     double w = 0.0;
@@ -1629,58 +1659,296 @@ __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& s
   __syncthreads();
 }
 
+// ---------------------------------------------------------------------------
+// Helpers. A workgroup whose group has no tree left helps a running group: it
+// takes a number in the group's helper count and then computes stripes of the
+// group's passes like a member. Member 0 reads the count in every batch and
+// reports it (capped at Gx - G) in its partial of pass 0, so every member
+// agrees on the contributors of the next batch; the number only grows, and a
+// helper once counted works in every later batch of that group. While the
+// group has helpers, member 0 publishes each batch in a descriptor of 13
+// 64-bit words, each holding the batch number in its high half, so a helper
+// knows it read one whole descriptor when all 13 numbers agree.
+// ---------------------------------------------------------------------------
+
+constexpr int kDescWords = 16;     // per group: 13 descriptor words, word 15 the helper count
+
+template <class PP>
+__device__ __forceinline__ uint64_t* ws_desc(const PP& P, int g) {
+  return reinterpret_cast<uint64_t*>(P.ws + P.off_desc) + static_cast<size_t>(g) * kDescWords;
+}
+template <class PP>
+__device__ __forceinline__ uint32_t* ws_hcount(const PP& P, int g) {
+  return reinterpret_cast<uint32_t*>(ws_desc(P, g) + 15);
+}
+
+constexpr uint32_t kDescDone = 1u << 31;
+
+// Member 0, thread 0: publishes batch `seq` of the tree in sm for helpers.
+template <int kCap>
+__device__ __forceinline__ void publish_batch(const Params& P, int g, uint32_t seq,
+                                              const Lds<TreeSmem<kCap>>& sm, int geff) {
+  uint64_t* d = ws_desc(P, g);
+  const uint64_t hi = static_cast<uint64_t>(seq) << 32;
+  const uint32_t w0 = static_cast<uint32_t>(sm.tree) | (static_cast<uint32_t>(sm.bn) << 20) |
+                      (static_cast<uint32_t>(geff) << 24);
+  st_rlx(&d[0], hi | w0);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int p = 2 * k + h;
+      const uint32_t e = p < sm.bn ? (static_cast<uint32_t>(sm.bnode[p]) & 0x7FFu) |
+                                         ((static_cast<uint32_t>(sm.bcmd[p]) & 0xFu) << 11)
+                                   : 0u;
+      v |= e << (16 * h);
+    }
+    st_rlx(&d[1 + k], hi | v);
+  }
+  const double prm[4] = {sm.cmd_ap, sm.cmd_bp, sm.cmd_cb, sm.cmd_cs};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint64_t b = static_cast<uint64_t>(__double_as_longlong(prm[k]));
+    st_rlx(&d[5 + 2 * k], hi | (b & 0xFFFFFFFFull));
+    st_rlx(&d[6 + 2 * k], hi | (b >> 32));
+  }
+}
+
+// Member 0, thread 0: the group has no tree left.
+template <class PP>
+__device__ __forceinline__ void publish_done(const PP& P, int g, uint32_t seq) {
+  st_rlx(&ws_desc(P, g)[0], (static_cast<uint64_t>(seq) << 32) | kDescDone);
+}
+
+// One pass of a stripe (all threads): STATS, or SPASS / WSUM weights.
+template <typename T, class A>
+__device__ __forceinline__ StripeResult stripe_pass(Lds<WgScratch>& ws, const T* rb, const T* rs,
+                                                    const Geom& geo, const SegRange& r, int cmd,
+                                                    const TermParams& tp, const A& ar) {
+  StripeResult part;
+  switch (cmd) {
+    case kCmdStats2: stripe_stats<T, A, true>(ws, rb, rs, geo, r, ar, part); break;
+    case kCmdStats1: stripe_stats<T, A, false>(ws, rb, rs, geo, r, ar, part); break;
+    default:
+      if (cmd == kCmdSPassSd) stripe_wsum<T, A, true>(ws, rb, rs, geo, r, ar, tp, part);
+      else stripe_wsum<T, A, false>(ws, rb, rs, geo, r, ar, tp, part);
+      break;
+  }
+  return part;
+}
+
+// Thread 0: writes contributor c's partials of batch `seq` (pass p's result
+// for p < bn, empty entries for the other passes so that every entry of the
+// parity buffer alternates its tag), then waits until they are performed.
+__device__ __forceinline__ void write_part(const Params& P, int g, uint32_t seq, int p, int c,
+                                           const StripeResult& r, uint64_t count) {
+  const uint64_t tag = batch_tag(seq);
+  SegPart* dst = ws_parts(P, g, static_cast<int>(seq & 1u), p) + c;
+  st_rlx(&dst->w[0], enc_sum(r.s0, tag));
+  st_rlx(&dst->w[1], enc_sum(r.s1, tag));
+  st_rlx(&dst->w[2], enc_max(r.m0, tag));
+  st_rlx(&dst->w[3], enc_max(r.m1, tag, count));
+}
+__device__ __forceinline__ void finish_parts(const Params& P, int g, uint32_t seq, int bn, int c) {
+  const StripeResult z{0.0, 0.0, 0.0f, 0.0f};
+  for (int p = bn; p < kMaxBatch; ++p) write_part(P, g, seq, p, c, z, 0);
+  // This batch's stores are performed before any store of the next batch is
+  // issued, so a reader that has seen this contributor's next partials will
+  // find these, not the ones from two uses earlier, which carry the same tag.
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+}
+
+// Waits (wave 0) for a descriptor of group g newer than `last`, or its end,
+// and copies it to LDS. ws.help_state: 0 new batch, 1 group done, 2 abandoned.
+__device__ __forceinline__ void await_desc(Lds<WgScratch>& ws, const Params& P, int g,
+                                           uint32_t last) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t* d = ws_desc(P, g);
+  const long long t0 = wall_clock64();
+  for (int it = 0;; ++it) {
+    const uint64_t w = lane < 13 ? ld_rlx(&d[lane]) : 0;
+    const uint64_t w0 = __shfl(w, 0, 64);
+    const uint32_t seq0 = static_cast<uint32_t>(w0 >> 32);
+    if (static_cast<uint32_t>(w0) & kDescDone) {
+      if (lane == 0) ws.help_state = 1;
+      return;
+    }
+    const bool same = lane >= 13 || static_cast<uint32_t>(w >> 32) == seq0;
+    if (__ballot(!same) == 0 && seq0 != last && seq0 != 0) {
+      const uint32_t lo = static_cast<uint32_t>(w);
+      if (lane == 0) {
+        ws.d_seq = seq0;
+        ws.d_tree = static_cast<int>(lo & 0xFFFFFu);
+        ws.d_bn = static_cast<int>((lo >> 20) & 0xFu);
+        ws.d_geff = static_cast<int>((lo >> 24) & 0x7Fu);
+        ws.help_state = 0;
+      }
+      if (lane >= 1 && lane <= 4) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t e = (lo >> (16 * h)) & 0xFFFFu;
+          ws.d_node[2 * (lane - 1) + h] = static_cast<int16_t>(e & 0x7FFu);
+          ws.d_cmd[2 * (lane - 1) + h] = static_cast<int8_t>((e >> 11) & 0xFu);
+        }
+      }
+      // parameters: lanes 5..12 hold the halves of ap, bp, cb, cs
+      const uint32_t lo_next = __shfl_down(lo, 1, 64);
+      if (lane >= 5 && lane <= 11 && ((lane - 5) & 1) == 0) {
+        const double v = __longlong_as_double(static_cast<long long>(
+            (static_cast<uint64_t>(lo_next) << 32) | lo));
+        const int k = (lane - 5) >> 1;
+        if (k == 0) ws.d_ap = v;
+        else if (k == 1) ws.d_bp = v;
+        else if (k == 2) ws.d_cb = v;
+        else ws.d_cs = v;
+      }
+      return;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    if ((it & 15) == 15) {
+      uint32_t ab = 0;
+      if (lane == 0) ab = ld_rlx(ws_abort(P));
+      if (__shfl(ab, 0, 64) || wall_clock64() - t0 > P.spin_limit) {
+        if (lane == 0) {
+          st_rlx(ws_abort(P), 1u);
+          ws.help_state = 2;
+        }
+        return;
+      }
+    }
+  }
+}
+
+// Contributor c of group g until the group has no tree left (all threads).
+// Returns false if the launch was abandoned.
+template <typename T, class A>
+__device__ __forceinline__ bool help_group(Lds<WgScratch>& ws, const Params& P, const A& ar, int g,
+                                           int c) {
+  const int tid = threadIdx.x;
+  uint32_t last = 0;
+  for (;;) {
+    if (tid < 64) await_desc(ws, P, g, last);
+    __syncthreads();
+    const int state = ws.help_state;
+    if (state != 0) return state == 1;
+    const uint32_t seq = ws.d_seq;
+    const int bn = ws.d_bn, geff = ws.d_geff, tree = ws.d_tree;
+    last = seq;
+    if (c < geff) {
+      const TermParams tp{ws.d_cb, ws.d_cs, ws.d_ap, ws.d_bp};
+      for (int p = 0; p < bn; ++p) {
+        const int node = ws.d_node[p];
+        const T* rb = row_ptr<T>(P, P.target, tree, node);
+        const T* rs = row_ptr<T>(P, P.draft, tree, node);
+        const Geom geo = row_geom(rb, P.vocab);
+        const StripeResult part = stripe_pass<T, A>(ws, rb, rs, geo, stripe(geo, c, geff),
+                                                    ws.d_cmd[p], tp, ar);
+        if (tid == 0) write_part(P, g, seq, p, c, part, 0);
+      }
+      if (tid == 0) finish_parts(P, g, seq, bn, c);
+    }
+    __syncthreads();
+  }
+}
+
+// A workgroup whose group is done (all threads): helps a running group with
+// the fewest helpers that still takes one, until none does. Workgroups that
+// look at the same time spread over the groups with that fewest count: each
+// starts its search at its own position.
+template <typename T, class A>
+__device__ __forceinline__ void help_others(Lds<WgScratch>& ws, const Params& P, A ar,
+                                            int g_self) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int cap = P.Gx - P.G;
+  const int ng = P.ngroups;
+  const uint32_t start = (static_cast<uint32_t>(blockIdx.x) * 2654435761u) % static_cast<uint32_t>(ng);
+  for (;;) {
+    if (tid < 64) {
+      // fewest helpers among the running groups that take one
+      uint32_t fewest = ~0u;
+      for (int gg = lane; gg < ng; gg += 64) {
+        if (gg == g_self) continue;
+        const uint64_t w0 = ld_rlx(&ws_desc(P, gg)[0]);
+        if (static_cast<uint32_t>(w0) & kDescDone) continue;
+        const uint32_t n = ld_rlx(ws_hcount(P, gg));
+        if (static_cast<int>(n) < cap && n < fewest) fewest = n;
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(fewest, off, 64);
+        fewest = o < fewest ? o : fewest;
+      }
+      // the first such group from this workgroup's starting position
+      uint32_t best = ~0u;    // distance from the start
+      if (fewest != ~0u) {
+        for (int j = lane; j < ng; j += 64) {
+          const int gg = static_cast<int>((start + static_cast<uint32_t>(j)) % static_cast<uint32_t>(ng));
+          if (gg == g_self) continue;
+          const uint64_t w0 = ld_rlx(&ws_desc(P, gg)[0]);
+          if (static_cast<uint32_t>(w0) & kDescDone) continue;
+          if (ld_rlx(ws_hcount(P, gg)) == fewest) {
+            best = static_cast<uint32_t>(j);
+            break;
+          }
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(best, off, 64);
+        best = o < best ? o : best;
+      }
+      if (lane == 0) {
+        int g2 = best == ~0u ? -1 : static_cast<int>((start + best) % static_cast<uint32_t>(ng));
+        int h = 0;
+        if (g2 >= 0) {
+          h = static_cast<int>(__hip_atomic_fetch_add(ws_hcount(P, g2), 1u, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT));
+          if (h >= cap) h = -1;          // taken meanwhile: look again
+        }
+        ws.help_g = g2;
+        ws.help_h = h;
+      }
+    }
+    __syncthreads();
+    const int g2 = ws.help_g, h = ws.help_h;
+    __syncthreads();
+    if (g2 < 0) return;                  // no group takes a helper
+    if (h < 0) continue;
+    if (!help_group<T, A>(ws, P, ar, g2, P.G + h)) return;
+  }
+}
+
 // This member's share of the batch in sm.b* (all threads): its stripe of every
-// pass, published as tagged partials. The members' partials are awaited in the
-// next controller step.
+// pass, published as tagged partials. The contributors' partials are awaited
+// in the next controller step.
 template <typename T, class A, int kCap>
 __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
                                           const Params& P, const A& ar, int g, int m) {
   const int tid = threadIdx.x;
   const int bn = sm.bn;
   const uint32_t seq = sm.seq + 1u;
-  const int par = static_cast<int>(seq & 1u);
-  const uint64_t tag = batch_tag(seq);
   const int b = sm.tree;
+  const int geff = sm.geff;
+  uint64_t hnext = 0;
+  if (m == 0 && tid == 0) {
+    if (geff > P.G) publish_batch(P, g, seq, sm, geff);
+    const int n = static_cast<int>(ld_rlx(ws_hcount(P, g)));
+    const int cap = P.Gx - P.G;
+    hnext = static_cast<uint64_t>(n < cap ? n : cap);
+  }
+  const TermParams tp{sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp};
   for (int p = 0; p < bn; ++p) {
     const int node = sm.bnode[p];
-    const int cmd = sm.bcmd[p];
     const T* rb = row_ptr<T>(P, P.target, b, node);
     const T* rs = row_ptr<T>(P, P.draft, b, node);
     const Geom geo = row_geom(rb, P.vocab);
-    const SegRange r = stripe(geo, m, P.G);
-    StripeResult part;
-    switch (cmd) {
-      case kCmdStats2: stripe_stats<T, A, true>(ws, rb, rs, geo, r, ar, part); break;
-      case kCmdStats1: stripe_stats<T, A, false>(ws, rb, rs, geo, r, ar, part); break;
-      default: {
-        const TermParams tp{sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp};
-        if (cmd == kCmdSPassSd) stripe_wsum<T, A, true>(ws, rb, rs, geo, r, ar, tp, part);
-        else stripe_wsum<T, A, false>(ws, rb, rs, geo, r, ar, tp, part);
-        break;
-      }
-    }
-    if (tid == 0) {
-      SegPart* dst = ws_parts(P, g, par, p) + m;
-      st_rlx(&dst->w[0], enc_sum(part.s0, tag));
-      st_rlx(&dst->w[1], enc_sum(part.s1, tag));
-      st_rlx(&dst->w[2], enc_max(part.m0, tag));
-      st_rlx(&dst->w[3], enc_max(part.m1, tag));
-    }
+    const StripeResult part = stripe_pass<T, A>(ws, rb, rs, geo, stripe(geo, m, geff),
+                                                sm.bcmd[p], tp, ar);
+    if (tid == 0) write_part(P, g, seq, p, m, part, p == 0 ? hnext : 0);
   }
   if (tid == 0) {
-    // The entries of the passes this batch does not have are written too, so
-    // that every entry of a parity buffer is rewritten at each use and its tag
-    // alternates: an entry left from two uses earlier would carry the tag the
-    // next reader expects.
-    for (int p = bn; p < kMaxBatch; ++p) {
-      SegPart* dst = ws_parts(P, g, par, p) + m;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) st_rlx(&dst->w[j], j < 2 ? enc_sum(0.0, tag) : enc_max(0.0f, tag));
-    }
-    // This batch's stores are performed before any store of the next batch is
-    // issued, so a member that has seen this member's next partials will find
-    // these, not the ones from two uses earlier, which carry the same tag.
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    finish_parts(P, g, seq, bn, m);
     sm.seq = seq;
     sm.pending = 1;
     // the weights of pass 0 stay available for drawing Y at its node
@@ -1706,6 +1974,9 @@ __global__ void __launch_bounds__(256) init_kernel(Params P) {
   uint64_t* parts = reinterpret_cast<uint64_t*>(P.ws + P.off_parts);
   for (size_t k = i; k < P.parts_words; k += static_cast<size_t>(gridDim.x) * blockDim.x)
     parts[k] = 0u;
+  uint64_t* desc = reinterpret_cast<uint64_t*>(P.ws + P.off_desc);
+  for (size_t k = i; k < P.desc_words; k += static_cast<size_t>(gridDim.x) * blockDim.x)
+    desc[k] = 0u;
   if (i < P.batch) {
     P.status[i] = TV_TREE_ABORTED;
     P.accept_len[i] = -1;
@@ -1728,12 +1999,13 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   if (tid == 0) {
     Ps_ = P;
     sm.seq = 0;
+    sm.geff = sm.geff_last = P.G;
     ws.stop = 0;
   }
   __syncthreads();
+  bool live = true;
   for (int b = g; b < P.batch; b += P.ngroups) {
     begin_tree<T>(sm, Ps, b);
-    bool live = true;
     for (;;) {
       controller_step<T, A>(sm, ws, Ps, ar, g, m);
       if (sm.cmd == kCmdDone) break;
@@ -1746,6 +2018,10 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
     if (!live) break;
     if (m == 0) finish_tree(sm, Ps);
   }
+  if (!live) return;
+  if (m == 0 && tid == 0) publish_done(P, g, sm.seq + 1u);
+  // the group has no tree left: help the groups that still run
+  if (P.Gx > P.G) help_others<T, A>(ws, P, ar, g);
 }
 
 // Vocabularies below this use the precise element path whatever the dtype:
@@ -1799,6 +2075,13 @@ int launch_typed(Params P, A ar, hipStream_t stream) {
   if (ngroups > P.batch) ngroups = P.batch;
   P.G = static_cast<int>(G);
   P.ngroups = static_cast<int>(ngroups);
+  // contributors a group's pass may have once helpers join: bounded so that
+  // groups times contributors stay within the partials' kMaxGrid slots
+  long long gmax = nvec / 512 < kMaxGroup ? nvec / 512 : kMaxGroup;
+  long long gx = tv::kMaxGrid / ngroups;
+  if (gx > gmax) gx = gmax;
+  if (gx < G) gx = G;
+  P.Gx = static_cast<int>(gx);
   P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s
   long long init_n = static_cast<long long>(P.parts_words);
   if (init_n < P.batch) init_n = P.batch;
@@ -1847,6 +2130,8 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   P.ws = static_cast<uint8_t*>(workspace);
   P.off_parts = L.off_parts;
   P.parts_words = L.parts_bytes / 8;
+  P.off_desc = L.off_desc;
+  P.desc_words = L.desc_bytes / 8;
   P.batch = a.batch;
   P.num_nodes = a.num_nodes;
   P.vocab = a.vocab;

@@ -36,14 +36,18 @@ struct VerifyArgs {
 constexpr int kMaxGrid = 4096;        // workgroups of one launch
 constexpr int kMaxGroup = 64;         // workgroups that verify one tree together
 constexpr int kMaxBatchPasses = 8;    // passes computed together for one tree
-constexpr int kSegPartBytes = 32;     // one member's partial result of one pass
+constexpr int kSegPartBytes = 32;     // one contributor's partial result of one pass
+constexpr int kGroupDescBytes = 128;  // a group's batch descriptor and helper count
 
-// Device workspace: a header (the abort flag) and the members' partial
-// results, double buffered by batch parity. Groups times members never exceed
-// kMaxGrid, nor batch times kMaxGroup.
+// Device workspace: a header (the abort flag), the contributors' partial
+// results, double buffered by batch parity, and one descriptor block per
+// group. Groups times contributors never exceed kMaxGrid, nor batch times
+// kMaxGroup.
 struct WorkspaceLayout {
-  size_t off_parts;        // partials [group][parity][pass][member]
+  size_t off_parts;        // partials [group][parity][pass][contributor]
   size_t parts_bytes;
+  size_t off_desc;         // per group: a batch descriptor for helpers and the helper count
+  size_t desc_bytes;
   size_t bytes;
 };
 
@@ -58,6 +62,10 @@ inline WorkspaceLayout workspace_layout(int32_t batch, int32_t vocab) {
   L.off_parts = off;
   L.parts_bytes = static_cast<size_t>(kSegPartBytes) * 2 * kMaxBatchPasses * (wg < 1 ? 1 : wg);
   off = align256(off + L.parts_bytes);
+  const int64_t groups = batch < kMaxGrid ? batch : kMaxGrid;
+  L.off_desc = off;
+  L.desc_bytes = static_cast<size_t>(kGroupDescBytes) * (groups < 1 ? 1 : groups);
+  off = align256(off + L.desc_bytes);
   L.bytes = off;
   return L;
 }
