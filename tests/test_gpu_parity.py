@@ -123,6 +123,20 @@ def test_configs_full_size(cfg, trees):
         torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("batch", [512, 1024])
+def test_large_batches_with_helpers(batch):
+    """Batches beyond one tree per group: groups of one workgroup, groups that
+    verify two trees in turn, and helpers joining running groups (sampled
+    trees, all statuses)."""
+    bt = W.make_batch(5, step=5, device=DEV, mode=W.WITHOUT_REPLACEMENT, batch=batch,
+                      vocab=16400)
+    gpu = parity.run_gpu(bt, False, False)
+    assert (gpu["status"] == tv.TV_TREE_OK).all()
+    trees = list(range(0, batch, batch // 48)) + [batch - 1]
+    rep = parity.check(bt, False, trees=trees, gpu=gpu, label=f"B{batch}")
+    assert_clean(rep, f"batch {batch}")
+
+
 # --------------------------------------------------------------------------
 # Edge cases
 # --------------------------------------------------------------------------
