@@ -54,9 +54,12 @@
 // to double). Members poll the G partials of a pass with agent-scope atomic
 // loads until all words carry the expected tag: 64-bit accesses are single-copy
 // atomic, so each word read is whole, and no counter, fence or second round of
-// loads is needed. Partials are double buffered by batch parity and the tag
-// alternates between the uses of a buffer: a member can only write batch k+2
-// after every member has written batch k+1, hence has read batch k. Every wait
+// loads is needed; agent-scope atomic loads see other workgroups' atomic
+// stores without a cache invalidation. Partials are double buffered by batch
+// parity and the tag alternates between the uses of a buffer; every entry is
+// rewritten at each use, and a contributor's stores of one batch are performed
+// before it issues the next batch's (its next exchange load waits for them),
+// so an entry left from two uses earlier is never read. Every wait
 // is bounded by a wall-clock limit after which the launch is abandoned (trees
 // not finished then report TV_TREE_ABORTED), so no wave can spin forever.
 #include <hip/hip_runtime.h>
@@ -299,6 +302,7 @@ struct WgScratch {
   double smp_window;        // mass of the window of chunks just scanned
   double smp_chunks[256];   // chunk sums of one window
   int hnext;                // helpers member 0 reported for the next batch
+  StripeResult res[kMaxBatch];   // this workgroup's results of the batch's passes
   // a helper's view of the group it helps
   int help_g, help_h, help_state;
   uint32_t d_seq;
@@ -1273,8 +1277,11 @@ __device__ __forceinline__ bool await_part(const PP& P, const SegPart* part, int
     if (lane < G) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) w[j] = ld_rlx(&part[lane].w[j]);
-      ok = tags_are(w, tag);
     }
+    // with the loads, this wave's stores of the last batch's partials are
+    // performed (the order the exchange relies on)
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    if (lane < G) ok = tags_are(w, tag);
     if (__ballot(!ok) == 0) return true;
     __builtin_amdgcn_s_sleep(1);
     if ((it & 15) == 15) {
@@ -1304,8 +1311,6 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
   const uint64_t tag = batch_tag(sm.seq);
   if (tid == 0) ws.stop = 0;
   __syncthreads();
-  // no line of the partials cached from an earlier batch is used
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   for (int p = wave; p < bn; p += kNW) {
     const int cmd = sm.bcmd[p];
     const int node = sm.bnode[p];
@@ -1740,7 +1745,9 @@ __device__ __forceinline__ StripeResult stripe_pass(Lds<WgScratch>& ws, const T*
 
 // Thread 0: writes contributor c's partials of batch `seq` (pass p's result
 // for p < bn, empty entries for the other passes so that every entry of the
-// parity buffer alternates its tag), then waits until they are performed.
+// parity buffer alternates its tag), then waits until they are performed. The
+// partials of a batch are written together at its end, so that no store is in
+// flight while the stripes run (the combine needs every pass anyway).
 __device__ __forceinline__ void write_part(const Params& P, int g, uint32_t seq, int p, int c,
                                            const StripeResult& r, uint64_t count) {
   const uint64_t tag = batch_tag(seq);
@@ -1750,13 +1757,19 @@ __device__ __forceinline__ void write_part(const Params& P, int g, uint32_t seq,
   st_rlx(&dst->w[2], enc_max(r.m0, tag));
   st_rlx(&dst->w[3], enc_max(r.m1, tag, count));
 }
-__device__ __forceinline__ void finish_parts(const Params& P, int g, uint32_t seq, int bn, int c) {
+__device__ __forceinline__ void write_parts(const Params& P, const Lds<WgScratch>& ws, int g,
+                                            uint32_t seq, int bn, int c, uint64_t count0) {
+  for (int p = 0; p < bn; ++p) {
+    const StripeResult r{ws.res[p].s0, ws.res[p].s1, ws.res[p].m0, ws.res[p].m1};
+    write_part(P, g, seq, p, c, r, p == 0 ? count0 : 0);
+  }
   const StripeResult z{0.0, 0.0, 0.0f, 0.0f};
   for (int p = bn; p < kMaxBatch; ++p) write_part(P, g, seq, p, c, z, 0);
-  // This batch's stores are performed before any store of the next batch is
-  // issued, so a reader that has seen this contributor's next partials will
-  // find these, not the ones from two uses earlier, which carry the same tag.
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  // The stores are not awaited here: the wave's next wait for a load of the
+  // exchange (the combine's or a helper's first poll) waits for them too, and
+  // it comes before any store of the next batch. So a reader that has seen
+  // this contributor's next partials will find these, not the ones from two
+  // uses earlier, which carry the same tag.
 }
 
 // Waits (wave 0) for a descriptor of group g newer than `last`, or its end,
@@ -1768,6 +1781,9 @@ __device__ __forceinline__ void await_desc(Lds<WgScratch>& ws, const Params& P, 
   const long long t0 = wall_clock64();
   for (int it = 0;; ++it) {
     const uint64_t w = lane < 13 ? ld_rlx(&d[lane]) : 0;
+    // with the loads, this wave's stores of the last batch's partials are
+    // performed (the order the exchange relies on)
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     const uint64_t w0 = __shfl(w, 0, 64);
     const uint32_t seq0 = static_cast<uint32_t>(w0 >> 32);
     if (static_cast<uint32_t>(w0) & kDescDone) {
@@ -1844,9 +1860,14 @@ __device__ __forceinline__ bool help_group(Lds<WgScratch>& ws, const Params& P, 
         const Geom geo = row_geom(rb, P.vocab);
         const StripeResult part = stripe_pass<T, A>(ws, rb, rs, geo, stripe(geo, c, geff),
                                                     ws.d_cmd[p], tp, ar);
-        if (tid == 0) write_part(P, g, seq, p, c, part, 0);
+        if (tid == 0) {
+          ws.res[p].s0 = part.s0;
+          ws.res[p].s1 = part.s1;
+          ws.res[p].m0 = part.m0;
+          ws.res[p].m1 = part.m1;
+        }
       }
-      if (tid == 0) finish_parts(P, g, seq, bn, c);
+      if (tid == 0) write_parts(P, ws, g, seq, bn, c, 0);
     }
     __syncthreads();
   }
@@ -1945,10 +1966,15 @@ __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     const Geom geo = row_geom(rb, P.vocab);
     const StripeResult part = stripe_pass<T, A>(ws, rb, rs, geo, stripe(geo, m, geff),
                                                 sm.bcmd[p], tp, ar);
-    if (tid == 0) write_part(P, g, seq, p, m, part, p == 0 ? hnext : 0);
+    if (tid == 0) {
+      ws.res[p].s0 = part.s0;
+      ws.res[p].s1 = part.s1;
+      ws.res[p].m0 = part.m0;
+      ws.res[p].m1 = part.m1;
+    }
   }
   if (tid == 0) {
-    finish_parts(P, g, seq, bn, m);
+    write_parts(P, ws, g, seq, bn, m, hnext);
     sm.seq = seq;
     sm.pending = 1;
     // the weights of pass 0 stay available for drawing Y at its node
@@ -2020,6 +2046,9 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   }
   if (!live) return;
   if (m == 0 && tid == 0) publish_done(P, g, sm.seq + 1u);
+  // no store in flight on the way into the helpers' stripes, which then wait
+  // for their loads one by one rather than for all at once
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   // the group has no tree left: help the groups that still run
   if (P.Gx > P.G) help_others<T, A>(ws, P, ar, g);
 }
