@@ -49,19 +49,19 @@
 // across members), so results are reproducible for a given group size.
 //
 // Synchronisation. A member writes each partial as four 64-bit words with
-// agent-scope atomic stores; every word carries the batch's tag bit (a spare
-// bit: the sign of a sum, the lowest mantissa bit of a float maximum widened
-// to double). Members poll the G partials of a pass with agent-scope atomic
-// loads until all words carry the expected tag: 64-bit accesses are single-copy
-// atomic, so each word read is whole, and no counter, fence or second round of
-// loads is needed; agent-scope atomic loads see other workgroups' atomic
-// stores without a cache invalidation. Partials are double buffered by batch
-// parity and the tag alternates between the uses of a buffer; every entry is
-// rewritten at each use, and a contributor's stores of one batch are performed
-// before it issues the next batch's (its next exchange load waits for them),
-// so an entry left from two uses earlier is never read. Every wait
-// is bounded by a wall-clock limit after which the launch is abandoned (trees
-// not finished then report TV_TREE_ABORTED), so no wave can spin forever.
+// agent-scope atomic stores; every word carries the batch's 16-bit tag (in the
+// lowest mantissa bits of a sum, in the zero low bits of a float maximum
+// widened to double). Members poll the G partials of a pass with agent-scope
+// atomic loads until all words carry the expected tag: 64-bit accesses are
+// single-copy atomic, so each word read is whole, and no counter, fence or
+// second round of loads is needed; agent-scope atomic loads see other
+// workgroups' atomic stores without a cache invalidation. Partials are double
+// buffered by batch parity, so batch k+1 never overwrites what a member may
+// still be reading of batch k, and every entry is rewritten at least every 14
+// batches, so an entry left from an earlier batch never carries the tag being
+// awaited. Every wait is bounded by a wall-clock limit after which the launch
+// is abandoned (trees not finished then report TV_TREE_ABORTED), so no wave
+// can spin forever.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -139,41 +139,42 @@ __device__ __forceinline__ Lds<X>& lds_ref(X& x) {
 
 // One contributor's partial result of one pass: four 64-bit words (two sums,
 // two maxima), each written and read with a single-copy atomic 64-bit access
-// and each carrying a 'written' bit and the batch's tag bit, so a reader that
-// sees both in all four words has the whole result of that batch. The sums
-// are >= 0 (or NaN): the tag is their sign bit and the written bit their last
-// mantissa bit (the sum loses that bit). The maxima are floats widened to
-// doubles, whose low 29 mantissa bits are 0: bit 0 is the written bit, bit 1
-// the tag, bits 2-7 carry a small count (member 0 reports the number of
-// helpers for the next batch in the draft maximum of pass 0).
+// and each carrying the batch's 16-bit tag, so a reader that sees the tag in
+// all four words has the whole result of that batch. The sums are >= 0 (or
+// NaN): the tag replaces their 16 lowest mantissa bits (a relative change
+// below 2^-36). The maxima are floats widened to doubles, whose low 29
+// mantissa bits are 0: bits 0-15 hold the tag, bits 16-21 a small count
+// (member 0 reports the number of helpers for the next batch in the draft
+// maximum of pass 0).
 struct SegPart {
   uint64_t w[4];
 };
 
-// Tag bit of batch `seq` (1, 2, ...): the two parity buffers are used by
-// batches 1, 3, 5, ... and 2, 4, 6, ...; the tag alternates between the uses
-// of a buffer, starting at 1 (buffers are cleared to 0 before each launch).
-__device__ __forceinline__ uint64_t batch_tag(uint32_t seq) { return ((seq + 1u) >> 1) & 1u; }
+// Tag of batch `seq` (1, 2, ...): never 0, the value of a cleared entry
+// (entries are cleared before each launch).
+__device__ __forceinline__ uint64_t batch_tag(uint32_t seq) {
+  return 0x8000u | (seq & 0x7FFFu);
+}
 
-constexpr uint64_t kSumMeta = (1ull << 63) | 1ull;
+constexpr uint64_t kTagMask = 0xFFFFull;
+constexpr uint64_t kMaxMeta = 0x3FFFFFull;     // tag and count bits of a maximum
 __device__ __forceinline__ uint64_t enc_sum(double v, uint64_t tag) {
-  return (static_cast<uint64_t>(__double_as_longlong(v)) & ~kSumMeta) | (tag << 63) | 1ull;
+  return (static_cast<uint64_t>(__double_as_longlong(v)) & ~kTagMask) | tag;
 }
 __device__ __forceinline__ double dec_sum(uint64_t w) {
-  return __longlong_as_double(static_cast<long long>(w & ~kSumMeta));
+  return __longlong_as_double(static_cast<long long>(w & ~kTagMask));
 }
 __device__ __forceinline__ uint64_t enc_max(float v, uint64_t tag, uint64_t count = 0) {
-  return static_cast<uint64_t>(__double_as_longlong(static_cast<double>(v))) | 1ull | (tag << 1) |
-         (count << 2);
+  return static_cast<uint64_t>(__double_as_longlong(static_cast<double>(v))) | tag |
+         (count << 16);
 }
 __device__ __forceinline__ float dec_max(uint64_t w) {
-  return static_cast<float>(__longlong_as_double(static_cast<long long>(w & ~0xFFull)));
+  return static_cast<float>(__longlong_as_double(static_cast<long long>(w & ~kMaxMeta)));
 }
-__device__ __forceinline__ int max_count(uint64_t w) { return static_cast<int>((w >> 2) & 63u); }
+__device__ __forceinline__ int max_count(uint64_t w) { return static_cast<int>((w >> 16) & 63u); }
 __device__ __forceinline__ bool tags_are(const uint64_t (&w)[4], uint64_t tag) {
-  const uint64_t mm = 1ull | (tag << 1);
-  return (w[0] & kSumMeta) == ((tag << 63) | 1ull) && (w[1] & kSumMeta) == ((tag << 63) | 1ull) &&
-         (w[2] & 3u) == mm && (w[3] & 3u) == mm;
+  return (w[0] & kTagMask) == tag && (w[1] & kTagMask) == tag && (w[2] & kTagMask) == tag &&
+         (w[3] & kTagMask) == tag;
 }
 
 // The sums and maxima a stripe pass produces.
@@ -1744,10 +1745,11 @@ __device__ __forceinline__ StripeResult stripe_pass(Lds<WgScratch>& ws, const T*
 }
 
 // Thread 0: writes contributor c's partials of batch `seq` (pass p's result
-// for p < bn, empty entries for the other passes so that every entry of the
-// parity buffer alternates its tag), then waits until they are performed. The
-// partials of a batch are written together at its end, so that no store is in
-// flight while the stripes run (the combine needs every pass anyway).
+// for p < bn), together at the end of the batch, so that no store is in
+// flight while the stripes run (the combine needs every pass anyway). One
+// entry p >= bn, chosen in turn, gets an empty partial, so that no entry is
+// more than 14 batches old: an entry left from an earlier batch never carries
+// the tag of the batch being read.
 __device__ __forceinline__ void write_part(const Params& P, int g, uint32_t seq, int p, int c,
                                            const StripeResult& r, uint64_t count) {
   const uint64_t tag = batch_tag(seq);
@@ -1763,13 +1765,11 @@ __device__ __forceinline__ void write_parts(const Params& P, const Lds<WgScratch
     const StripeResult r{ws.res[p].s0, ws.res[p].s1, ws.res[p].m0, ws.res[p].m1};
     write_part(P, g, seq, p, c, r, p == 0 ? count0 : 0);
   }
-  const StripeResult z{0.0, 0.0, 0.0f, 0.0f};
-  for (int p = bn; p < kMaxBatch; ++p) write_part(P, g, seq, p, c, z, 0);
+  const int pd = 1 + static_cast<int>((seq >> 1) % (kMaxBatch - 1));
+  if (pd >= bn) write_part(P, g, seq, pd, c, StripeResult{0.0, 0.0, 0.0f, 0.0f}, 0);
   // The stores are not awaited here: the wave's next wait for a load of the
   // exchange (the combine's or a helper's first poll) waits for them too, and
-  // it comes before any store of the next batch. So a reader that has seen
-  // this contributor's next partials will find these, not the ones from two
-  // uses earlier, which carry the same tag.
+  // it comes before any store of the next batch.
 }
 
 // Waits (wave 0) for a descriptor of group g newer than `last`, or its end,
