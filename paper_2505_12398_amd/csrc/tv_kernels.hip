@@ -304,6 +304,7 @@ struct WgScratch {
   double smp_chunks[256];   // chunk sums of one window
   int hnext;                // helpers member 0 reported for the next batch
   StripeResult res[kMaxBatch];   // this workgroup's results of the batch's passes
+  uint64_t res_count;            // the count member 0 reports with them
   // a helper's view of the group it helps
   int help_g, help_h, help_state;
   uint32_t d_seq;
@@ -709,6 +710,7 @@ struct TreeSmem {
   double A[kCap];                  // residual target b = [A p - B q]_+
   double B[kCap];
   double rem[kCap];                // draft mass left after removing rejected tokens
+  double removed[kCap];            // draft terms of the rejected children's tokens
   double pini[kCap];
   double sdsum[kCap];              // sum of the draft row's terms in its frame
   double invsb[kCap];              // 1 / (sum of the target row's terms)
@@ -756,20 +758,21 @@ __device__ inline double child_rate(const Lds<TreeSmem<kCap>>& sm, int mode, int
   return fmin(sm.pi[j] * v, 1.0);
 }
 
-// After a pass at j that rejected a child: draft mass left once every rejected
+// After a pass at j that rejected child l: draft mass left once every rejected
 // child's token is removed (Eq. e2 applied to all of them), from the pass's own
-// draft-term sum minus those tokens' terms, computed the same way.
+// draft-term sum minus those tokens' terms, computed the same way. Children
+// are rejected in index order, so the running sum adds their terms in that
+// order.
 template <int kCap>
-__device__ inline void update_remaining_mass(Lds<TreeSmem<kCap>>& sm, int j,
+__device__ inline void update_remaining_mass(Lds<TreeSmem<kCap>>& sm, int j, int l,
                                              bool pass_summed_draft) {
   if (pass_summed_draft) {
     sm.sdsum[j] = sm.res_sd;
     sm.flags[j] |= kFlagSd;
   }
   const double total = sm.sdsum[j];
-  double removed = 0.0;
-  const int s0 = sm.child_start[j];
-  for (int r = 0; r < sm.next_child[j]; ++r) removed += sm.et[sm.child_list[s0 + r]];
+  const double removed = sm.removed[j] + sm.et[l];
+  sm.removed[j] = removed;
   sm.rem[j] = (total - removed) / total;
 }
 
@@ -848,6 +851,7 @@ __device__ inline void init_node_state(Lds<TreeSmem<kCap>>& sm, int c, double pi
   sm.A[c] = 1.0;
   sm.B[c] = 0.0;
   sm.rem[c] = 1.0;
+  sm.removed[c] = 0.0;
 }
 
 struct TraversalArgs {
@@ -987,7 +991,7 @@ __device__ __forceinline__ void advance_impl(Lds<TreeSmem<kCap>>& sm, TraversalA
         } else {
           sm.pi[j] = 0.0;
         }
-        if (wo) update_remaining_mass(sm, j, summed_draft);
+        if (wo) update_remaining_mass(sm, j, l, summed_draft);
         ct.cur = j;
         ct.phase = kPhDescend;
         continue;
@@ -1042,7 +1046,7 @@ __device__ __forceinline__ void advance_impl(Lds<TreeSmem<kCap>>& sm, TraversalA
         const double inv = 1.0 / S;
         sm.A[j] = ct.alpha * inv;
         sm.B[j] = ct.beta * inv;
-        if (wo) update_remaining_mass(sm, j, summed_draft);
+        if (wo) update_remaining_mass(sm, j, c, summed_draft);
         ct.phase = kPhTlVisit;
         continue;
       }
@@ -1627,17 +1631,24 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
 }
 
 // One controller step (all threads; every member of the group runs it on the
-// same data): combine the completed batch, then advance the traversal until it
-// needs the next batch or the tree is done. Only member 0 draws Y.
+// same data): publish this member's partials of the completed batch, combine
+// everyone's, then advance the traversal until it needs the next batch, a
+// local sample or the tree is done. With `after_sample`, only advance past the
+// local sample just drawn (member 0 draws Y; the caller runs the sample, so
+// that this function makes no call and keeps its return address in place).
+// The partials are stored here rather than at the end of the batch: a call
+// first waits for every memory access in flight, and stores issued inside it
+// are awaited together with the first poll of the combine instead.
 template <typename T, class A, int kCap>
 __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& sm,
                                                           Lds<WgScratch>& ws,
                                                           const Lds<Params>& P, A ar, int g,
-                                                          int m) {
+                                                          int m, bool after_sample) {
   const int tid = threadIdx.x;
   if (sm.status == TV_TREE_OK) {
-    int done_cmd = kCmdNone;
-    if (sm.pending) {
+    int done_cmd = after_sample ? kCmdLocalSample : kCmdNone;
+    if (!after_sample && sm.pending) {
+      if (tid == 0) write_parts(P, ws, g, sm.seq, sm.bn, m, ws.res_count);
       if (!combine<T, A>(sm, ws, P, ar, g)) {   // the launch was abandoned
         if (tid == 0) sm.cmd = kCmdAbandon;
         __syncthreads();
@@ -1646,18 +1657,10 @@ __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& s
       done_cmd = sm.bcmd[0];
       if (tid == 0) sm.pending = 0;
     }
-    for (;;) {
-      if (tid == 0) {
-        __builtin_amdgcn_s_setprio(3);
-        advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
-        __builtin_amdgcn_s_setprio(0);
-      }
-      __syncthreads();
-      if (sm.cmd != kCmdLocalSample) break;
-      if (m == 0) local_sample<T, A>(sm, ws, P, ar, g);
-      else if (tid == 0) sm.res_y = 0;   // Y is reported by member 0
-      __syncthreads();
-      done_cmd = kCmdLocalSample;
+    if (tid == 0) {
+      __builtin_amdgcn_s_setprio(3);
+      advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
+      __builtin_amdgcn_s_setprio(0);
     }
   } else if (tid == 0) {
     sm.cmd = kCmdDone;
@@ -1750,7 +1753,8 @@ __device__ __forceinline__ StripeResult stripe_pass(Lds<WgScratch>& ws, const T*
 // entry p >= bn, chosen in turn, gets an empty partial, so that no entry is
 // more than 14 batches old: an entry left from an earlier batch never carries
 // the tag of the batch being read.
-__device__ __forceinline__ void write_part(const Params& P, int g, uint32_t seq, int p, int c,
+template <class PP>
+__device__ __forceinline__ void write_part(const PP& P, int g, uint32_t seq, int p, int c,
                                            const StripeResult& r, uint64_t count) {
   const uint64_t tag = batch_tag(seq);
   SegPart* dst = ws_parts(P, g, static_cast<int>(seq & 1u), p) + c;
@@ -1759,7 +1763,8 @@ __device__ __forceinline__ void write_part(const Params& P, int g, uint32_t seq,
   st_rlx(&dst->w[2], enc_max(r.m0, tag));
   st_rlx(&dst->w[3], enc_max(r.m1, tag, count));
 }
-__device__ __forceinline__ void write_parts(const Params& P, const Lds<WgScratch>& ws, int g,
+template <class PP>
+__device__ __forceinline__ void write_parts(const PP& P, const Lds<WgScratch>& ws, int g,
                                             uint32_t seq, int bn, int c, uint64_t count0) {
   for (int p = 0; p < bn; ++p) {
     const StripeResult r{ws.res[p].s0, ws.res[p].s1, ws.res[p].m0, ws.res[p].m1};
@@ -1941,8 +1946,8 @@ __device__ __forceinline__ void help_others(Lds<WgScratch>& ws, const Params& P,
 }
 
 // This member's share of the batch in sm.b* (all threads): its stripe of every
-// pass, published as tagged partials. The contributors' partials are awaited
-// in the next controller step.
+// pass, left in LDS. The next controller step publishes them as tagged
+// partials and awaits the other contributors'.
 template <typename T, class A, int kCap>
 __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
                                           const Params& P, const A& ar, int g, int m) {
@@ -1974,7 +1979,7 @@ __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     }
   }
   if (tid == 0) {
-    write_parts(P, ws, g, seq, bn, m, hnext);
+    ws.res_count = hnext;      // the partials are written by the next controller step
     sm.seq = seq;
     sm.pending = 1;
     // the weights of pass 0 stay available for drawing Y at its node
@@ -2033,7 +2038,13 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   for (int b = g; b < P.batch; b += P.ngroups) {
     begin_tree<T>(sm, Ps, b);
     for (;;) {
-      controller_step<T, A>(sm, ws, Ps, ar, g, m);
+      controller_step<T, A>(sm, ws, Ps, ar, g, m, false);
+      while (sm.cmd == kCmdLocalSample) {
+        if (m == 0) local_sample<T, A>(sm, ws, Ps, ar, g);
+        else if (tid == 0) sm.res_y = 0;   // Y is reported by member 0
+        __syncthreads();
+        controller_step<T, A>(sm, ws, Ps, ar, g, m, true);
+      }
       if (sm.cmd == kCmdDone) break;
       if (sm.cmd == kCmdAbandon) {
         live = false;
