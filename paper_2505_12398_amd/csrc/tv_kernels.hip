@@ -1372,14 +1372,18 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
     const int next = P.G + ws.hnext;
     sm.geff = next > G ? next : G;
   }
-  // children's original ratios r0 = p(x)/q(x) and draft terms
+  // children's original ratios r0 = p(x)/q(x) and draft terms: 32 threads per
+  // pass (a node with bad statistics gets values it never uses: the traversal
+  // fails the tree before it reads them)
   const double kd = ar.kd();
-  for (int p = 0; p < bn; ++p) {
+  static_assert(kMaxBatch * 32 <= kNT, "one thread group of 32 per pass");
+  if (tid < bn * 32) {
+    const int p = tid >> 5;
     const int node = sm.bnode[p];
-    if (sm.bcmd[p] != kCmdStats2 || (sm.flags[node] & kFlagBad)) continue;
+    const bool stats2 = sm.bcmd[p] == kCmdStats2;
     const double Cb = sm.cb[node], Cs = sm.cs[node];
     const double norm = sm.invsb[node] / sm.invss[node];   // ts / tb
-    for (int i = tid; i < sm.child_count[node]; i += kNT) {
+    for (int i = tid & 31; stats2 && i < sm.child_count[node]; i += 32) {
       const int c = sm.child_list[sm.child_start[node] + i];
       const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb);
       const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs);
