@@ -260,3 +260,23 @@ def test_deterministic():
     for k in a:
         if a[k] is not None:
             assert np.array_equal(a[k], b[k]), k
+
+
+def test_repeated_launches_with_helpers_agree():
+    """The full 256-tree, V=128256 batch, launched several times: helpers join
+    at timing-dependent points, so the last bits of the sums may differ, but
+    every decision, accepted node, Y and status must be the same, and the
+    acceptance probabilities the same to well within the fp32 tolerance."""
+    bt = W.make_batch(5, step=7, device=DEV, mode=W.WITHOUT_REPLACEMENT, batch=256)
+    runs = [parity.run_gpu(bt, False) for _ in range(4)]
+    a = runs[0]
+    assert (a["status"] == tv.TV_TREE_OK).all()
+    for b in runs[1:]:
+        for k in ("status", "accept_len", "accepted_node", "bonus_token", "node_state"):
+            assert np.array_equal(a[k], b[k]), k
+        th_a, th_b = a["node_theta"], b["node_theta"]
+        assert np.allclose(th_a, th_b, rtol=1e-6, atol=1e-9)
+    rep = parity.check(bt, False, trees=[0, 85, 170, 255], gpu=a, label="repeat")
+    assert_clean(rep, "repeated launches")
+    del bt
+    torch.cuda.empty_cache()
