@@ -26,23 +26,25 @@
  *
  * Memory and streams. Every pointer is a device pointer. The caller owns all
  * buffers, including a device workspace of tv_workspace_size() bytes that the
- * call uses as scratch (per-group counters and the partial sums of every
- * vocabulary pass; its contents need no initialisation and are meaningless
- * afterwards). The library
+ * call uses as scratch (the partial sums of every vocabulary pass and one
+ * batch descriptor per group; its contents need no initialisation and are
+ * meaningless afterwards). The library
  * allocates nothing, keeps no state between calls and never synchronises the
  * host: work is enqueued on `stream` and the call returns. Inputs are
  * read-only. Outputs are written for every tree, including trees whose status
  * is not TV_TREE_OK (they get -1 sentinels). Calls that write the same output
  * buffers or share a workspace must be ordered by the caller.
  *
- * Execution. One call makes one cooperative launch of at most as many
- * workgroups as the device holds at once, in groups that each verify one tree
- * at a time (several workgroups per tree when the batch is small). The
- * members of a group exchange partial sums through the workspace and wait for
- * each other at every vocabulary pass; the launch waits until the whole grid
- * can be resident. Every wait inside the kernel is bounded: a call that makes
- * no progress for 4 seconds gives up and reports TV_TREE_ABORTED for the
- * trees it did not finish.
+ * Execution. One call enqueues a small initialisation kernel and one
+ * cooperative launch of at most as many workgroups as the device holds at
+ * once, in groups that each verify one tree at a time (several workgroups per
+ * tree; three per tree at 256 trees on MI355X). The members of a group
+ * exchange partial sums through the workspace and wait for each other at
+ * every vocabulary pass; a group with no tree left lends its workgroups to
+ * running groups. The launch waits until the whole grid can be resident.
+ * Every wait inside the kernel is bounded: a call that makes no progress for
+ * 4 seconds gives up and reports TV_TREE_ABORTED for the trees it did not
+ * finish.
  *
  * Errors. Argument problems the host can see (null pointers, sizes, enums,
  * temperature, misaligned pointers) return a tv_status_t other than TV_OK and
