@@ -75,6 +75,13 @@ class TreeResult:
     residual_passes: int = 0       # Eq. (e1)-(e3) updates executed
     leaf_accepted: int = 0         # 1 if the accepted node has no children in the input tree
     tests: int = 0                 # nodes compared against a uniform
+    # Early rejection (bookkeeping for verifiers that skip updates that decide
+    # nothing): a rejection that removes the last remaining child of a non-root
+    # node j while u[j] >= p(j) needs no update at j, since Eq. (e3) never
+    # raises p(j) (S <= p(j) by Eq. (e1)), so j is rejected whatever S is.
+    early_rejections: int = 0      # updates a verifier with early rejection skips
+    early_margin: float = float("inf")  # min |u[j] - p(j)| over the rule's checks
+    early_nodes: list = field(default_factory=list)  # the j of each skipped update
     test_order: list = field(default_factory=list)
     margins: dict = field(default_factory=dict)   # node -> |u - theta| for tested nodes
     y_weights: np.ndarray = None   # distribution Y is drawn from
@@ -83,6 +90,13 @@ class TreeResult:
     @property
     def counters(self):
         return (self.rows_consulted, self.residual_passes, self.leaf_accepted, self.tests)
+
+    @property
+    def counters_early(self):
+        """Counters of a verifier that applies early rejection: the same, with
+        only the residual updates it executes."""
+        return (self.rows_consulted, self.residual_passes - self.early_rejections,
+                self.leaf_accepted, self.tests)
 
 
 # ---------------------------------------------------------------------------
@@ -321,6 +335,8 @@ def verify_tree(parents, tokens, target_logits, draft_logits, temperature, unifo
             break
         res.node_state[leaf] = NODE_REJECTED
         alive[leaf] = False                 # T <- T - {X_gamma}
+        if uniforms is not None:
+            _early_rejection(res, children, alive, p, uniforms, j)
 
         # Residual and draft distributions at the parent, Eq. (e1) and (e2).
         d, S = residual_e1(p[j], b[j], s[j])
@@ -346,6 +362,21 @@ def verify_tree(parents, tokens, target_logits, draft_logits, temperature, unifo
         if res.y_weights is None:
             return _error(TREE_NONFINITE, n1)
     return _finish(res, children, depth, parents, uniforms)
+
+
+def _early_rejection(res: TreeResult, children, alive, p, uniforms, j):
+    """Counts the update at j as one an early-rejecting verifier skips when j
+    is not the root, j has no remaining child, and u[j] >= p(j) before the
+    update. p(j) only falls under Eq. (e3): S = sum [p(j) b - s]_+ <= p(j)
+    (Eq. (e1)) and S / (S + 1 - p(j)) grows with S, reaching p(j) at S = p(j).
+    So j, tested next, is rejected whatever S is."""
+    if j == 0 or any(alive[c] for c in children[j]):
+        return
+    u = float(uniforms[j])
+    res.early_margin = min(res.early_margin, abs(u - float(p[j])))
+    if u >= p[j]:
+        res.early_rejections += 1
+        res.early_nodes.append(j)
 
 
 def rerate_chains(p, b, s, parents, tokens, alive, j):

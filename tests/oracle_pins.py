@@ -313,10 +313,67 @@ def pin_invariants():
         assert sn[x] == 0.0 and abs(sn.sum() - 1.0) < 1e-12
 
 
+def pin_early_rejection_worked_example():
+    """Sec. 3.2 with every drafted node rejected: after X4, the last child of X1,
+    is rejected, p(X1) = 1/11 <= u, and X1 is then rejected (its rate falls to
+    0): that update is the one an early-rejecting verifier skips. After X5, the
+    only child of X2, p(X2) = 1 > u and X2 is accepted: that update is needed
+    (it gives Y's residual). Updates after X3 (X4 still remains) and at the root
+    never qualify."""
+    par, tok, zb, zs, T = W.worked_example()
+    u = np.full(6, ALMOST_ONE, np.float32)
+    u[0] = 0.5
+    r = O.verify_tree(par, tok, zb, zs, T, u, O.WITHOUT_REPLACEMENT)
+    assert r.residual_passes == 4, r.residual_passes      # after X3, X4, X1, X5
+    assert r.early_nodes == [1], r.early_nodes
+    assert r.counters_early[1] == 3
+    # the rule's checks: u(X1) - 1/11 and 1 - u(X2) = 2^-24
+    _close(r.early_margin, 2.0 ** -24, 1e-18, "early margin")
+    # X1 tested with u just above its rate: not skipped, same decisions
+    u[1] = np.float32(1.0 / 11.0) * np.float32(0.5)
+    r2 = O.verify_tree(par, tok, zb, zs, T, u, O.WITHOUT_REPLACEMENT)
+    assert r2.early_nodes == [] and r2.test_order == r.test_order
+
+
+def pin_early_rejection_sound():
+    """Every update counted as skippable is followed by the rejection of its
+    node with theta <= u (p never rises under Eq. e3), on random irregular trees
+    in both sibling modes; and such updates occur."""
+    rng = np.random.default_rng(21)
+    seen = 0
+    for t in range(120):
+        V = int(rng.integers(3, 12))
+        par = W.geometric_bfs_parents(rng, 12, 4)
+        n1 = len(par)
+        zb = rng.normal(0.0, 2.0, (n1, V))
+        zs = zb + rng.normal(0.0, 1.5, (n1, V))
+        mode = O.WITHOUT_REPLACEMENT if t % 2 == 0 else O.WITH_REPLACEMENT
+        tok = np.zeros(n1, np.int64)
+        for j in range(n1):
+            kids = [i for i in range(n1) if par[i] == j]
+            if kids:
+                q = np.exp(zs[j] - zs[j].max())
+                q /= q.sum()
+                pick = rng.choice(V, size=len(kids), replace=(mode == O.WITH_REPLACEMENT
+                                                              or len(kids) > V), p=q)
+                tok[kids] = pick
+        u = (rng.integers(0, 2 ** 24, n1) * 2.0 ** -24).astype(np.float32)
+        r = O.verify_tree(par, tok, zb, zs, 1.0, u, mode)
+        if r.status != O.TREE_OK:
+            continue
+        for j in r.early_nodes:
+            seen += 1
+            assert j != 0
+            assert r.node_state[j] == O.NODE_REJECTED, (t, j)
+            assert r.node_theta[j] <= float(u[j]), (t, j, r.node_theta[j], u[j])
+        assert r.counters_early[1] == r.residual_passes - len(r.early_nodes)
+    assert seen > 20, seen
+
+
 FAST_PINS = [pin_worked_example_trace, pin_worked_example_tokenlevel, pin_worked_example_law,
              pin_single_token_table1, pin_rrsw_example, pin_tempered_softmax_inverse,
              pin_inverse_cdf_law, pin_identical_models, pin_depth1_equals_rrsw,
-             pin_invariants]
+             pin_invariants, pin_early_rejection_worked_example, pin_early_rejection_sound]
 ENUM_PINS = [pin_lossless_exact, pin_lossless_irregular_T07, pin_chain_optimality]
 ALL_PINS = FAST_PINS + ENUM_PINS
 

@@ -82,6 +82,20 @@ def _residual_without_norm(b, s):
     return np.maximum(b - s, 0.0)
 
 
+def _early_when_below(res, children, alive, p, uniforms, j):
+    if j == 0 or any(alive[c] for c in children[j]):
+        return
+    if float(uniforms[j]) < p[j]:       # comparison the wrong way round
+        res.early_rejections += 1
+        res.early_nodes.append(j)
+
+
+def _early_any_child(res, children, alive, p, uniforms, j):
+    if j != 0 and float(uniforms[j]) >= p[j]:   # ignores the children still left
+        res.early_rejections += 1
+        res.early_nodes.append(j)
+
+
 MUTATIONS = {
     "e1 drops the p factor": ("residual_e1", _e1_without_p),
     "e1 target and draft swapped": ("residual_e1", _e1_swapped),
@@ -95,6 +109,8 @@ MUTATIONS = {
     "temperature ignored": ("tempered_softmax", _softmax_no_temperature),
     "children visited last-first": ("_structure", _structure_reversed),
     "RRS residual not normalised": ("rrs_residual", _residual_without_norm),
+    "early rejection with u below p": ("_early_rejection", _early_when_below),
+    "early rejection with children left": ("_early_rejection", _early_any_child),
 }
 
 
