@@ -71,9 +71,9 @@ def algorithmic_bytes(counters, vocab, elem_bytes, num_nodes):
 TV_NUM_COUNTERS = 4
 
 
-def cpu_baseline(batch, gpu_out, sample: int, workers: int):
+def cpu_baseline(batch, gpu_outs: dict, sample: int, workers: int):
     """The oracle on the first `sample` trees of one step, on host cores, with
-    parity of those trees against the GPU outputs."""
+    parity of those trees against each of the GPU outputs (by label)."""
     import multiprocessing as mp
 
     import numpy as np
@@ -90,20 +90,23 @@ def cpu_baseline(batch, gpu_out, sample: int, workers: int):
     with mp.get_context("fork").Pool(workers) as pool:
         refs = pool.map(_oracle_one, args)
     dt = time.perf_counter() - t0
-    g = parity.host_outputs(gpu_out)
-    rep = parity.ParityReport()
-    for b, ref in enumerate(refs):
-        kind, msg, worst = parity.compare_tree(g, b, ref, False, False, "bf16")
-        rep.trees += 1
-        rep.max_theta_rel = max(rep.max_theta_rel, worst[0])
-        rep.max_theta_abs = max(rep.max_theta_abs, worst[1])
-        if kind == "exact":
-            rep.exact += 1
-        elif kind == "near_tie":
-            rep.near_ties += 1
-        else:
-            rep.failures.append(f"tree {b}: {msg}")
-    return sample / dt, dt, rep
+    reps = {}
+    for label, gpu_out in gpu_outs.items():
+        g = parity.host_outputs(gpu_out)
+        rep = parity.ParityReport()
+        for b, ref in enumerate(refs):
+            kind, msg, worst = parity.compare_tree(g, b, ref, False, False, "bf16")
+            rep.trees += 1
+            rep.max_theta_rel = max(rep.max_theta_rel, worst[0])
+            rep.max_theta_abs = max(rep.max_theta_abs, worst[1])
+            if kind == "exact":
+                rep.exact += 1
+            elif kind == "near_tie":
+                rep.near_ties += 1
+            else:
+                rep.failures.append(f"{label} tree {b}: {msg}")
+        reps[label] = rep
+    return sample / dt, dt, reps
 
 
 def _oracle_one(args):
@@ -263,22 +266,31 @@ def main():
         workers = args.cpu_workers or min(16, os.cpu_count() or 1)
         sample = min(args.cpu_sample, B)
         batch, _ = last
-        out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"],
-                              batch["draft"], batch["temperature"], batch["uniforms"], mode,
-                              want_nodes=True, want_counters=True)
+        # the timed configuration (no theta output: early rejection), with node
+        # states for the comparison; and once more with theta, for its accuracy
+        outs = {theta: tv.verify_batch(batch["parents"], batch["tokens"], batch["target"],
+                                       batch["draft"], batch["temperature"], batch["uniforms"],
+                                       mode, want_nodes=True, want_theta=theta,
+                                       want_counters=True)
+                for theta in (False, True)}
         torch.cuda.synchronize()
-        tps, secs, rep = cpu_baseline(batch, out, sample, workers)
+        tps, secs, reps = cpu_baseline(batch, {"timed": outs[False], "theta": outs[True]},
+                                       sample, workers)
         res["cpu_baseline"] = {
             "value": tps, "unit": "trees/s", "cores": workers, "kind": "oracle",
             "sample": f"first {sample} trees of timed step {args.steps - 1} "
                       f"({secs:.1f} s wall, float64 numpy, one process per core)",
         }
+        rep, rth = reps["timed"], reps["theta"]
         res["parity_sample"] = {"trees": rep.trees, "exact": rep.exact,
                                 "near_ties": rep.near_ties, "failures": len(rep.failures),
-                                "max_theta_rel_err": rep.max_theta_rel,
-                                "max_theta_abs_err": rep.max_theta_abs}
-        if rep.failures:
-            print("\n".join(rep.failures[:5]), file=sys.stderr)
+                                "with_theta": {"exact": rth.exact, "near_ties": rth.near_ties,
+                                               "failures": len(rth.failures),
+                                               "max_theta_rel_err": rth.max_theta_rel,
+                                               "max_theta_abs_err": rth.max_theta_abs}}
+        for r in (rep, rth):
+            if r.failures:
+                print("\n".join(r.failures[:5]), file=sys.stderr)
     print(json.dumps(res), flush=True)
 
 

@@ -158,13 +158,19 @@ size_t tv_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab);
  *   status         int32 [batch]   TV_TREE_*
  *   node_state     int8  [batch][num_nodes] or NULL   TV_NODE_*
  *   node_theta     float [batch][num_nodes] or NULL   acceptance probability the node was
- *                  tested with; 0 for pruned nodes, -1 for untested nodes
+ *                  tested with; 0 for pruned nodes, -1 for untested nodes.
+ *                  When NULL, tv_verify applies early rejection: a node's rate never
+ *                  rises under Eq. (e3) (S <= p by Eq. e1), so when the last child of a
+ *                  non-root node j is rejected while u[j] >= p(j), j is rejected without
+ *                  its update (one pass over j's rows fewer). Every other output is the
+ *                  same either way; only j's exact theta is then never computed.
  *   p_init         float [batch][num_nodes] or NULL   Alg. 3 initial chain rates p^ini.
  *                  Asking for them makes the verifier read the rows of every node that
  *                  has children, which the traversal itself may not need.
  *   counters       int32 [batch][TV_NUM_COUNTERS] or NULL:
  *                  [0] nodes whose target and draft rows were read for the traversal,
- *                  [1] residual updates (Eq. e1-e3; one pass over both rows of the parent),
+ *                  [1] residual updates executed (Eq. e1-e3; one pass over both rows of
+ *                      the parent; without the ones early rejection skips),
  *                  [2] 1 if the accepted node has no children (its target row is read for Y),
  *                  [3] nodes tested against their uniform
  *   workspace      device buffer of at least tv_workspace_size() bytes, 256-byte aligned

@@ -141,10 +141,12 @@ class VerifyOutputs:
 def verify_batch(parents, tokens, target_logits, draft_logits, temperature, uniforms, mode,
                  tokenlevel=False, want_nodes=True, want_p_init=False, want_counters=True,
                  out: VerifyOutputs | None = None, stream=None,
-                 workspace=None) -> VerifyOutputs:
+                 workspace=None, want_theta=None) -> VerifyOutputs:
     """Allocate outputs and the workspace (torch, same device) unless given,
     check shapes, call the C entry point on the current stream and raise on a
-    non-OK return."""
+    non-OK return. ``want_nodes`` asks for node states and (unless
+    ``want_theta`` is False) the tested probabilities; without the latter,
+    tv_verify skips the residual updates that decide nothing."""
     import torch
     B, n1 = parents.shape
     V = target_logits.shape[-1]
@@ -171,7 +173,7 @@ def verify_batch(parents, tokens, target_logits, draft_logits, temperature, unif
             bonus_token=torch.empty(B, **i32), status=torch.empty(B, **i32),
             node_state=torch.empty((B, n1), dtype=torch.int8, device=dev) if want_nodes else None,
             node_theta=torch.empty((B, n1), dtype=torch.float32, device=dev)
-            if want_nodes else None,
+            if (want_nodes if want_theta is None else want_theta) else None,
             p_init=torch.empty((B, n1), dtype=torch.float32, device=dev) if want_p_init else None,
             counters=torch.empty((B, TV_NUM_COUNTERS), **i32) if want_counters else None)
     if stream is None:

@@ -121,6 +121,7 @@ struct Params {
   int vocab;
   int mode;
   int algo;
+  int early;                 // skip updates that decide nothing (node_theta not asked for)
   int G;                     // workgroups per group (per tree)
   int Gx;                    // most contributors (members + helpers) a group's pass has
   int ngroups;               // groups; group g verifies trees g, g + ngroups, ...
@@ -855,7 +856,7 @@ __device__ inline void init_node_state(Lds<TreeSmem<kCap>>& sm, int c, double pi
 }
 
 struct TraversalArgs {
-  int num_nodes, mode, algo;
+  int num_nodes, mode, algo, early;
 };
 
 struct Ctl {
@@ -967,6 +968,17 @@ __device__ __forceinline__ void advance_impl(Lds<TreeSmem<kCap>>& sm, TraversalA
         }
         sm.state[l] = TV_NODE_REJECTED;
         ++sm.next_child[j];
+        if (P.early && j != 0 && sm.next_child[j] == sm.child_count[j] &&
+            static_cast<double>(sm.u[j]) >= sm.pi[j]) {
+          // Early rejection: l was j's last child and j is tested next. Eq. (e3)
+          // never raises j's rate (S <= p by Eq. e1), so u[j] >= p already
+          // rejects j, whatever the update would give; the update, which only
+          // j's own test and a residual at j could use, is skipped. The test
+          // below records the current p as theta (an upper bound), which is
+          // why this applies only when theta is not an output.
+          ct.cur = j;
+          continue;
+        }
         const double cc = wo ? 1.0 / sm.rem[j] : 1.0;
         ct.alpha = sm.pi[j] * sm.A[j];
         ct.beta = sm.pi[j] * sm.B[j] + cc;
@@ -1663,7 +1675,7 @@ __device__ __attribute__((noinline)) void controller_step(Lds<TreeSmem<kCap>>& s
     }
     if (tid == 0) {
       __builtin_amdgcn_s_setprio(3);
-      advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo}, done_cmd);
+      advance(sm, TraversalArgs{P.num_nodes, P.mode, P.algo, P.early}, done_cmd);
       __builtin_amdgcn_s_setprio(0);
     }
   } else if (tid == 0) {
@@ -2181,6 +2193,7 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   P.vocab = a.vocab;
   P.mode = a.mode;
   P.algo = static_cast<int>(algo);
+  P.early = a.node_theta == nullptr ? 1 : 0;
   P.k64 = 1.4426950408889634 / static_cast<double>(a.temperature);
   P.k32 = static_cast<float>(P.k64);
   const bool precise = a.dtype == TV_DTYPE_F32 || a.vocab < kPreciseBelowVocab;

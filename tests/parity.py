@@ -8,6 +8,11 @@ if u*W lies within 1e-6*W of a CDF boundary. Any other difference is a
 failure. Acceptance probabilities (theta of tested nodes, p_init) must agree
 within 1e-5 relative for float32 logits and 2e-3 relative for bfloat16 logits
 (plus 1e-7 absolute for values near zero).
+
+Outputs without theta come from tv_verify with early rejection: their residual
+update counter is compared with the oracle's count of executed updates under
+that rule; a difference there is a near-tie if the rule's own comparison
+u[j] >= p(j) had an oracle margin below 1e-6.
 """
 
 from __future__ import annotations
@@ -72,15 +77,20 @@ def compare_tree(g: dict, b: int, ref, tokenlevel: bool, check_p_init: bool,
         ok = (g["accept_len"][b] == -1 and g["accepted_node"][b] == -1
               and g["bonus_token"][b] == -1)
         return ("exact", "", worst) if ok else ("fail", "error tree without sentinels", worst)
-    state, theta = g["node_state"][b], g["node_theta"][b]
+    state = g["node_state"][b]
+    theta = None if g["node_theta"] is None else g["node_theta"][b]
+    early = theta is None and not tokenlevel
     for node in ref.test_order:
         want = ref.node_state[node]
         if state[node] != want:
             if ref.margins[node] < BAND:
                 return "near_tie", f"node {node} margin {ref.margins[node]:.2e}", worst
+            gth = "-" if theta is None else f"{theta[node]:.9g}"
             return ("fail", f"node {node} state gpu {state[node]} oracle {want} "
-                    f"theta gpu {theta[node]:.9g} oracle {ref.node_theta[node]:.9g} "
+                    f"theta gpu {gth} oracle {ref.node_theta[node]:.9g} "
                     f"u-margin {ref.margins[node]:.2e}", worst)
+        if theta is None:
+            continue
         th_r = float(ref.node_theta[node])
         err = abs(float(theta[node]) - th_r)
         worst[1] = max(worst[1], err)
@@ -90,19 +100,25 @@ def compare_tree(g: dict, b: int, ref, tokenlevel: bool, check_p_init: bool,
             return "fail", f"node {node} theta gpu {theta[node]!r} oracle {th_r!r}", worst
     if not np.array_equal(state.astype(np.int64), ref.node_state.astype(np.int64)):
         return "fail", f"node states differ: gpu {state.tolist()} oracle {ref.node_state.tolist()}", worst
-    pruned = ref.node_state == tv.TV_NODE_PRUNED
-    if not np.all(theta[pruned] == 0.0):
-        return "fail", "pruned nodes must report theta 0", worst
-    untested = ref.node_state == tv.TV_NODE_UNTESTED
-    if not np.all(theta[untested] == -1.0):
-        return "fail", "untested nodes must report theta -1", worst
+    if theta is not None:
+        pruned = ref.node_state == tv.TV_NODE_PRUNED
+        if not np.all(theta[pruned] == 0.0):
+            return "fail", "pruned nodes must report theta 0", worst
+        untested = ref.node_state == tv.TV_NODE_UNTESTED
+        if not np.all(theta[untested] == -1.0):
+            return "fail", "untested nodes must report theta -1", worst
     if int(g["accepted_node"][b]) != ref.accepted_node or int(g["accept_len"][b]) != ref.accept_len:
         return ("fail", f"accepted gpu {g['accepted_node'][b]}/{g['accept_len'][b]} oracle "
                 f"{ref.accepted_node}/{ref.accept_len}", worst)
     if g["counters"] is not None:
-        want = np.array(ref.counters)
-        if not np.array_equal(g["counters"][b], want):
-            return "fail", f"counters gpu {g['counters'][b].tolist()} oracle {want.tolist()}", worst
+        want = np.array(ref.counters_early if early else ref.counters)
+        got = g["counters"][b]
+        if not np.array_equal(got, want):
+            others = [k for k in range(len(want)) if k != 1]
+            if (early and ref.early_margin < BAND
+                    and np.array_equal(got[others], want[others])):
+                return "near_tie", f"early rejection margin {ref.early_margin:.2e}", worst
+            return "fail", f"counters gpu {got.tolist()} oracle {want.tolist()}", worst
     if check_p_init and g["p_init"] is not None and not tokenlevel:
         for i, (a, r) in enumerate(zip(g["p_init"][b], ref.p_init)):
             if not _theta_ok(a, r, rtol):
@@ -121,19 +137,21 @@ def oracle_tree(batch: dict, b: int, tokenlevel: bool):
     return fn(par, tok, zb, zs, batch["temperature"], u, batch["mode"])
 
 
-def run_gpu(batch: dict, tokenlevel: bool, p_init: bool = False):
+def run_gpu(batch: dict, tokenlevel: bool, p_init: bool = False, theta: bool = True):
+    """Runs a verifier on the whole batch; without ``theta`` tv_verify applies
+    early rejection."""
     out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"], batch["draft"],
                           batch["temperature"], batch["uniforms"], batch["mode"],
-                          tokenlevel=tokenlevel, want_p_init=p_init)
+                          tokenlevel=tokenlevel, want_p_init=p_init, want_theta=theta)
     return host_outputs(out)
 
 
 def check(batch: dict, tokenlevel: bool, trees=None, p_init: bool = False,
-          gpu: dict | None = None, label: str = "") -> ParityReport:
+          gpu: dict | None = None, label: str = "", theta: bool = True) -> ParityReport:
     """Run the HIP verifier on the whole batch (unless ``gpu`` outputs are
     given) and compare the listed trees (all by default) with the oracle."""
     if gpu is None:
-        gpu = run_gpu(batch, tokenlevel, p_init)
+        gpu = run_gpu(batch, tokenlevel, p_init, theta)
     B = batch["parents"].shape[0]
     rep = ParityReport()
     for b in (range(B) if trees is None else trees):

@@ -52,6 +52,15 @@ def test_worked_example(tokenlevel):
         assert list(g["node_state"][0]) == [0, 2, 1, 2, 2, 2]
         np.testing.assert_allclose(g["node_theta"][0], [-1, 0, 1, 2 / 3, 7 / 11, 1 / 2],
                                    rtol=1e-6)
+        # updates after X3, X4, X1 and X5 (counter 1)
+        assert g["counters"][0][1] == 4
+        # without theta: the update after X4 is skipped (p(X1) = 1/11 <= u(X1))
+        rep = parity.check(batch, False, label="worked-early", theta=False)
+        assert_clean(rep, "worked example, early rejection")
+        g = parity.run_gpu(batch, False, theta=False)
+        assert g["node_theta"] is None
+        assert list(g["node_state"][0]) == [0, 2, 1, 2, 2, 2]
+        assert g["counters"][0][1] == 3
 
 
 @pytest.mark.parametrize("tokenlevel", [False, True])
@@ -75,6 +84,9 @@ def test_tiny_context_model(mode, tokenlevel):
                               mode, DEV)
     rep = parity.check(batch, tokenlevel, p_init=not tokenlevel, label="tiny")
     assert_clean(rep, f"tiny mode={mode} tokenlevel={tokenlevel}")
+    if not tokenlevel:
+        rep = parity.check(batch, False, label="tiny-early", theta=False)
+        assert_clean(rep, f"tiny mode={mode} early rejection")
 
 
 # --------------------------------------------------------------------------
@@ -90,6 +102,9 @@ def test_configs_reduced(cfg, vocab, batch, mode, tokenlevel):
     bt = W.make_batch(cfg, step=1, device=DEV, mode=mode, batch=batch, vocab=vocab)
     rep = parity.check(bt, tokenlevel, p_init=not tokenlevel, label=f"cfg{cfg}")
     assert_clean(rep, f"cfg{cfg} V={vocab} mode={mode} tokenlevel={tokenlevel}")
+    if not tokenlevel:
+        rep = parity.check(bt, False, label=f"cfg{cfg}-early", theta=False)
+        assert_clean(rep, f"cfg{cfg} V={vocab} mode={mode} early rejection")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -119,6 +134,8 @@ def test_configs_full_size(cfg, trees):
         for tl in (False, True):
             rep = parity.check(bt, tl, trees=trees, label=f"cfg{cfg}-full")
             assert_clean(rep, f"cfg{cfg} full mode={mode} tokenlevel={tl}")
+        rep = parity.check(bt, False, trees=trees, label=f"cfg{cfg}-full-early", theta=False)
+        assert_clean(rep, f"cfg{cfg} full mode={mode} early rejection")
         del bt
         torch.cuda.empty_cache()
 
@@ -135,6 +152,9 @@ def test_large_batches_with_helpers(batch):
     trees = list(range(0, batch, batch // 48)) + [batch - 1]
     rep = parity.check(bt, False, trees=trees, gpu=gpu, label=f"B{batch}")
     assert_clean(rep, f"batch {batch}")
+    gpu = parity.run_gpu(bt, False, False, theta=False)
+    rep = parity.check(bt, False, trees=trees, gpu=gpu, label=f"B{batch}-early", theta=False)
+    assert_clean(rep, f"batch {batch} early rejection")
 
 
 # --------------------------------------------------------------------------
