@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
 SLEEP_CYCLES = 2_000_000     # about 1 ms of GPU clock ahead of each timed launch
 CFG = 5
-PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "tv_verify_cfg5_hbm_counters.md")
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "tv_verify_256trees_n64_v128256_hbm_counters.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2505_12398_amd", "csrc", "tv_kernels.hip")
 METRIC = ("verified trees/sec + achieved HBM GB/s (% peak), 64-node trees, V=128256, bf16")
 
