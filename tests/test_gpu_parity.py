@@ -191,6 +191,9 @@ def test_root_only_and_tiny_vocab(tokenlevel):
         bt = _rand_batch(rng, par, vocab)
         rep = parity.check(bt, tokenlevel, p_init=not tokenlevel, label=f"small V{vocab}")
         assert_clean(rep, f"small tree V={vocab}")
+        if not tokenlevel:
+            rep = parity.check(bt, False, label=f"small V{vocab} early", theta=False)
+            assert_clean(rep, f"small tree V={vocab} early rejection")
 
 
 def test_large_trees():
@@ -207,6 +210,9 @@ def test_large_trees():
         bt = _rand_batch(rng, par, 64, mode=W.WITH_REPLACEMENT, scale=0.3)
         rep = parity.check(bt, tl, label="large")
         assert_clean(rep, f"1024-node trees tokenlevel={tl}")
+        if not tl:
+            rep = parity.check(bt, False, label="large-early", theta=False)
+            assert_clean(rep, "1024-node trees, early rejection")
 
 
 def test_identical_models_accept_first_leaf():
