@@ -13,6 +13,9 @@ Contents:
   written step by step with explicit V-vectors in float64.
 * :mod:`oracle.enumerate` -- exact output laws by enumerating every draft tree
   and every accept/reject branch (checks the losslessness theorem, Sec. 3.3).
+* :mod:`oracle.draft_sampler` -- the tokens of a draft tree drawn from each
+  parent's tempered draft distribution, with or without replacement
+  (Def. de_tree, Sec. 3.3), by inverse CDF at given uniforms.
 
 Pins (what the oracle is checked against, independent of itself) live in
 ``tests/test_oracle_*.py`` and ``tests/golden/``. Every function here is pinned;

@@ -18,6 +18,7 @@ import numpy as np
 
 import oracle.tv_oracle as O
 import oracle.enumerate as E
+import oracle.draft_sampler as DS
 import workloads as W
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
@@ -370,10 +371,62 @@ def pin_early_rejection_sound():
     assert seen > 20, seen
 
 
+def pin_draft_sampler_law():
+    """Def. de_tree: two children of the root drawn from the tempered Table 1
+    draft [.6, .3, .1] at T = 0.7. Over a 200 x 200 grid of uniforms the joint
+    frequency of the two tokens matches q(x1) q(x2) / (1 - q(x1)) without
+    replacement and q(x1) q(x2) with replacement (each inverse-CDF interval is
+    matched to within one grid step, so 3/200 bounds the error)."""
+    q0 = np.array([0.6, 0.3, 0.1])
+    T = 0.7
+    q = q0 ** (1.0 / np.float64(np.float32(T)))
+    q /= q.sum()
+    zs = np.tile(np.log(q0), (3, 1))
+    par = np.array([-1, 0, 0])
+    M = 200
+    grid = (np.arange(M) + 0.5) / M
+    for mode in (O.WITHOUT_REPLACEMENT, O.WITH_REPLACEMENT):
+        f = np.zeros((3, 3))
+        for u1 in grid:
+            for u2 in grid:
+                r = DS.draw_tree_tokens(par, zs, T, np.array([0.5, u1, u2]), mode)
+                assert r.status == O.TREE_OK and r.tokens[0] == -1
+                f[r.tokens[1], r.tokens[2]] += 1.0 / (M * M)
+        for a in range(3):
+            for b in range(3):
+                if mode == O.WITHOUT_REPLACEMENT:
+                    want = 0.0 if a == b else q[a] * q[b] / (1.0 - q[a])
+                else:
+                    want = q[a] * q[b]
+                assert abs(f[a, b] - want) <= 3.0 / M, (mode, a, b, f[a, b], want)
+
+
+def pin_draft_sampler_statuses():
+    """Error cases of the sampler: a parent link that does not point backwards,
+    a NaN in a row with children, and more children than tokens without
+    replacement (fine with replacement)."""
+    zs = np.zeros((4, 2))
+    u = np.full(4, 0.5)
+    r = DS.draw_tree_tokens(np.array([-1, 0, 3, 1]), zs, 1.0, u)
+    assert r.status == O.TREE_BAD_PARENT and np.all(r.tokens == -1)
+    bad = zs.copy()
+    bad[0, 1] = np.nan
+    r = DS.draw_tree_tokens(np.array([-1, 0, 0, 0]), bad, 1.0, u)
+    assert r.status == O.TREE_NONFINITE
+    r = DS.draw_tree_tokens(np.array([-1, 0, 0, 0]), zs, 1.0, u, O.WITHOUT_REPLACEMENT)
+    assert r.status == O.TREE_DEGENERATE
+    r = DS.draw_tree_tokens(np.array([-1, 0, 0, 0]), zs, 1.0, u, O.WITH_REPLACEMENT)
+    assert r.status == O.TREE_OK and list(r.tokens) == [-1, 1, 1, 1]
+    # two children at V = 2 without replacement take both tokens
+    r = DS.draw_tree_tokens(np.array([-1, 0, 0, 1]), zs, 1.0, u, O.WITHOUT_REPLACEMENT)
+    assert r.status == O.TREE_OK and sorted(r.tokens[1:3]) == [0, 1]
+
+
 FAST_PINS = [pin_worked_example_trace, pin_worked_example_tokenlevel, pin_worked_example_law,
              pin_single_token_table1, pin_rrsw_example, pin_tempered_softmax_inverse,
              pin_inverse_cdf_law, pin_identical_models, pin_depth1_equals_rrsw,
-             pin_invariants, pin_early_rejection_worked_example, pin_early_rejection_sound]
+             pin_invariants, pin_early_rejection_worked_example, pin_early_rejection_sound,
+             pin_draft_sampler_law, pin_draft_sampler_statuses]
 ENUM_PINS = [pin_lossless_exact, pin_lossless_irregular_T07, pin_chain_optimality]
 ALL_PINS = FAST_PINS + ENUM_PINS
 

@@ -171,3 +171,25 @@ def test_two_leaf_sibling_counterexample(monkeypatch):
     bad = first_token(E.draft_tree_law(O.verify_tree, par, M(), 1.0, O.WITH_REPLACEMENT,
                                        O.WITHOUT_REPLACEMENT, length=1))
     np.testing.assert_allclose(bad, [3 / 10, 17 / 50, 9 / 25], atol=1e-12)
+
+
+def _sampler_with_replacement(parents, draft_logits, temperature, uniforms, mode=0):
+    import oracle.draft_sampler as DS
+    return _draw_orig(parents, draft_logits, temperature, uniforms, O.WITH_REPLACEMENT)
+
+
+def _sampler_no_temperature(parents, draft_logits, temperature, uniforms, mode=0):
+    return _draw_orig(parents, draft_logits, 1.0, uniforms, mode)
+
+
+import oracle.draft_sampler as _DS  # noqa: E402
+
+_draw_orig = _DS.draw_tree_tokens
+
+
+@pytest.mark.parametrize("fn", [_sampler_with_replacement, _sampler_no_temperature])
+def test_sampler_mutation_is_caught(monkeypatch, fn):
+    """The sampler pins catch siblings drawn with replacement where they must
+    not repeat, and an ignored temperature."""
+    monkeypatch.setattr(_DS, "draw_tree_tokens", fn)
+    assert P.first_failure([P.pin_draft_sampler_law, P.pin_draft_sampler_statuses]) is not None
