@@ -203,6 +203,36 @@ int tv_verify_tokenlevel(int32_t batch, int32_t num_nodes, int32_t vocab,
                          float* p_init, int32_t* counters, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Draft-tree token sampler: the step that builds the trees tv_verify checks.
+ * A draft tree (Def. de_tree, Sec. 3.3) gives the children of every node
+ * tokens drawn from the draft model's distribution at that node,
+ * softmax(draft_logits[b][j] / temperature), with or without replacement.
+ * The children of a node are drawn in ascending node index, child c by the
+ * inverse CDF in ascending token order at uniforms[b][c]
+ * (y = min{y : u*W < C(y)}, W the row's total weight). Without replacement,
+ * each drawn token is removed before the next sibling's draw (the draft step
+ * of Eq. (e2)), so siblings never repeat. Uniforms come from the caller, like
+ * tv_verify's.
+ *
+ * Inputs (device, row-major, contiguous): parents int32 [batch][num_nodes]
+ * (parents[b][0] = -1, 0 <= parents[b][i] < i); draft_logits dtype
+ * [batch][num_nodes][vocab] (rows of nodes without children are not read);
+ * uniforms float32 [batch][num_nodes], each in [0, 1) (u[b][0] unused);
+ * temperature, vocab and mode as for tv_verify.
+ * Outputs (device): tokens int32 [batch][num_nodes] (tokens[b][0] = -1; every
+ * token -1 for a tree whose status is not TV_TREE_OK); status int32 [batch]:
+ * TV_TREE_OK, TV_TREE_BAD_PARENT, TV_TREE_NONFINITE (a row with children has
+ * NaN, +inf or no finite entry) or TV_TREE_DEGENERATE (without replacement, a
+ * node has more children than tokens of positive probability); the largest
+ * code found when there are several. No workspace; nothing is allocated.
+ * Returns a tv_status_t; argument errors launch nothing.
+ */
+int tv_draft_tokens(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
+                    const void* draft_logits, int32_t dtype, float temperature,
+                    const float* uniforms, int32_t mode, int32_t* tokens, int32_t* status,
+                    hipStream_t stream);
+
 /* Static, human-readable name of a tv_status_t value ("unknown status" otherwise). */
 const char* tv_status_string(int code);
 

@@ -41,6 +41,14 @@ _VERIFY_ARGTYPES = [
 ]
 
 
+_SAMPLE_ARGTYPES = [
+    ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,            # batch, num_nodes, vocab
+    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,          # parents, draft, dtype
+    ctypes.c_float, ctypes.c_void_p, ctypes.c_int32,           # temperature, uniforms, mode
+    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,         # tokens, status, stream
+]
+
+
 def load_library(path: str = LIB_PATH):
     """Load libtv.so once. Raises if it is not built."""
     global _lib
@@ -54,6 +62,8 @@ def load_library(path: str = LIB_PATH):
             fn = getattr(lib, name)
             fn.argtypes = _VERIFY_ARGTYPES
             fn.restype = ctypes.c_int
+        lib.tv_draft_tokens.argtypes = _SAMPLE_ARGTYPES
+        lib.tv_draft_tokens.restype = ctypes.c_int
         lib.tv_status_string.argtypes = [ctypes.c_int]
         lib.tv_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -116,6 +126,42 @@ def tv_verify_tokenlevel(batch, num_nodes, vocab, parents, tokens, target_logits
                  target_logits, draft_logits, dtype, temperature, uniforms, mode, accept_len,
                  accepted_node, bonus_token, status, node_state, node_theta, p_init, counters,
                  workspace, workspace_bytes, stream)
+
+
+def tv_draft_tokens(batch, num_nodes, vocab, parents, draft_logits, dtype, temperature,
+                    uniforms, mode, tokens, status, stream=None) -> int:
+    """C-ABI ``tv_draft_tokens``: pointers may be torch tensors or raw ints;
+    returns the status."""
+    return int(load_library().tv_draft_tokens(
+        int(batch), int(num_nodes), int(vocab), _ptr(parents), _ptr(draft_logits), int(dtype),
+        float(temperature), _ptr(uniforms), int(mode), _ptr(tokens), _ptr(status),
+        _ptr(stream)))
+
+
+def draft_tokens(parents, draft_logits, temperature, uniforms, mode, stream=None):
+    """Draws the tokens of a batch of draft trees on the device (torch tensors
+    in, (tokens, status) int32 tensors out); raises on a non-OK return."""
+    import torch
+    B, n1 = parents.shape
+    V = draft_logits.shape[-1]
+    dev = draft_logits.device
+    for name, t, shape in (("parents", parents, (B, n1)), ("uniforms", uniforms, (B, n1)),
+                           ("draft_logits", draft_logits, (B, n1, V))):
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+        if t.device != dev or not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous on {dev}")
+    if parents.dtype != torch.int32 or uniforms.dtype != torch.float32:
+        raise TypeError("parents must be int32 and uniforms float32")
+    tokens = torch.empty((B, n1), dtype=torch.int32, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream if dev.type == "cuda" else None
+    st = tv_draft_tokens(B, n1, V, parents, draft_logits, _dtype_code(draft_logits), temperature,
+                         uniforms, mode, tokens, status, stream)
+    if st != TV_OK:
+        raise TvError(st, "tv_draft_tokens")
+    return tokens, status
 
 
 def workspace_tensor(batch: int, num_nodes: int, vocab: int, device):

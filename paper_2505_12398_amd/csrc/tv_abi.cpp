@@ -40,6 +40,27 @@ int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
   return TV_OK;
 }
 
+int validate_sample(const SampleArgs& a) {
+  if (a.batch < 0 || a.num_nodes < 1 || a.vocab < 2) return TV_ERR_INVALID_ARG;
+  if (a.dtype != TV_DTYPE_BF16 && a.dtype != TV_DTYPE_F32) return TV_ERR_INVALID_ARG;
+  if (a.mode != TV_SIBLINGS_WITHOUT_REPLACEMENT && a.mode != TV_SIBLINGS_WITH_REPLACEMENT)
+    return TV_ERR_INVALID_ARG;
+  if (!(a.temperature > 0.0f) || !isfinite(a.temperature)) return TV_ERR_INVALID_ARG;
+  if (a.temperature < TV_MIN_TEMPERATURE || a.temperature > TV_MAX_TEMPERATURE)
+    return TV_ERR_UNSUPPORTED;
+  if (a.batch > TV_MAX_BATCH || a.num_nodes > TV_MAX_NODES || a.vocab > TV_MAX_VOCAB)
+    return TV_ERR_UNSUPPORTED;
+  if (a.dtype == TV_DTYPE_F32 && a.vocab > TV_MAX_VOCAB_F32) return TV_ERR_UNSUPPORTED;
+  if (a.batch == 0) return TV_OK;
+  if (!a.parents || !a.draft || !a.uniforms || !a.tokens || !a.status) return TV_ERR_INVALID_ARG;
+  const size_t esize = a.dtype == TV_DTYPE_BF16 ? 2 : 4;
+  if (reinterpret_cast<uintptr_t>(a.draft) % esize) return TV_ERR_INVALID_ARG;
+  const void* int_ptrs[] = {a.parents, a.uniforms, a.tokens, a.status};
+  for (const void* p : int_ptrs)
+    if (reinterpret_cast<uintptr_t>(p) % 4) return TV_ERR_INVALID_ARG;
+  return TV_OK;
+}
+
 }  // namespace tv
 
 namespace {
@@ -96,6 +117,17 @@ int tv_verify_tokenlevel(int32_t batch, int32_t num_nodes, int32_t vocab,
                        target_logits, draft_logits, dtype, temperature, uniforms, mode,
                        accept_len, accepted_node, bonus_token, status, node_state, node_theta,
                        p_init, counters, workspace, workspace_bytes, stream);
+}
+
+int tv_draft_tokens(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
+                    const void* draft_logits, int32_t dtype, float temperature,
+                    const float* uniforms, int32_t mode, int32_t* tokens, int32_t* status,
+                    hipStream_t stream) {
+  const tv::SampleArgs a{batch, num_nodes, vocab, parents, draft_logits, dtype, temperature,
+                         uniforms, mode, tokens, status};
+  const int st = tv::validate_sample(a);
+  if (st != TV_OK || batch == 0) return st;
+  return tv::launch_sample(a, stream);
 }
 
 const char* tv_status_string(int code) {

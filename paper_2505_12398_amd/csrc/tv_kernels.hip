@@ -2163,6 +2163,241 @@ int launch_cap(const Params& P, bool precise, hipStream_t stream) {
   return launch_typed<T, PreciseArith, kCap>(P, PreciseArith{P.k64}, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Draft-tree token sampler (Def. de_tree, Sec. 3.3): the children of every
+// node take tokens drawn from the node's tempered draft distribution, in
+// ascending node index, each by inverse CDF (ascending token order) at its own
+// uniform; without replacement, each drawn token is removed before the next
+// sibling's draw. One workgroup per (tree, node) row.
+// ---------------------------------------------------------------------------
+
+struct SampleParams {
+  const int32_t* parents;
+  const void* draft;
+  const float* uniforms;
+  int32_t* tokens;
+  int32_t* status;
+  int batch, num_nodes, vocab, mode;
+};
+
+struct SampleSmem {
+  int32_t kids[TV_MAX_NODES];      // children of the row's node, ascending
+  int32_t removed[TV_MAX_NODES];   // tokens drawn so far at this row (without replacement)
+  int nkids, nremoved, owner, token;
+  double W;
+};
+
+// Every tree starts OK with the root's token -1; the rows then raise status.
+__global__ void __launch_bounds__(256) sample_init_kernel(SampleParams S) {
+  const int b = static_cast<int>(blockIdx.x * blockDim.x + threadIdx.x);
+  if (b < S.batch) {
+    S.status[b] = TV_TREE_OK;
+    S.tokens[static_cast<size_t>(b) * S.num_nodes] = -1;
+  }
+}
+
+// Every token of a tree whose status is an error becomes -1.
+__global__ void __launch_bounds__(256) sample_finish_kernel(SampleParams S) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<size_t>(S.batch) * S.num_nodes) return;
+  if (S.status[i / S.num_nodes] != TV_TREE_OK) S.tokens[i] = -1;
+}
+
+// The weights of one row are 2^(z*k + c) in the frame c of its maximum,
+// grouped in units: head elements (up to the first 16-byte boundary),
+// 16-byte vectors, tail elements, in token order. A unit's sum and the running
+// sum inside it are formed in the same order, so a rescan reproduces the sums
+// that chose it. Tokens already drawn (without replacement) weigh 0.
+template <typename T, class A>
+struct RowWeights {
+  static constexpr int E = Elem<T>::E;
+  const T* row;
+  Geom g;
+  A ar;
+  double c;
+  const Lds<SampleSmem>* sm;
+
+  __device__ int units() const { return g.head + g.nvec + g.tail; }
+  __device__ int first(int u) const {
+    if (u < g.head) return u;
+    if (u < g.head + g.nvec) return g.head + (u - g.head) * E;
+    return g.head + g.nvec * E + (u - g.head - g.nvec);
+  }
+  __device__ int count(int u) const { return (u >= g.head && u < g.head + g.nvec) ? E : 1; }
+  __device__ bool drawn(int x) const {
+    for (int r = 0; r < sm->nremoved; ++r)
+      if (sm->removed[r] == x) return true;
+    return false;
+  }
+  __device__ void load(int u, float (&x)[E]) const {
+    if (count(u) == E) {
+      Elem<T>::unpack(load16(row, g.head, u - g.head), x);
+    } else {
+      x[0] = Elem<T>::scalar(row + first(u));
+    }
+  }
+  // weight of element e of unit u with value z
+  __device__ typename Terms<A, false, false>::W weight(int x, float z) const {
+    using W = typename Terms<A, false, false>::W;
+    if (sm->nremoved && drawn(x)) return W(0);
+    if constexpr (A::kPrecise) return ar.ex(z, c);
+    else return fast_exp2(fmaf(z, ar.k, static_cast<float>(c)));
+  }
+  __device__ double unit_sum(int u) const {
+    using W = typename Terms<A, false, false>::W;
+    float x[E];
+    load(u, x);
+    const int n = count(u), x0 = first(u);
+    W acc = W(0);
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (e < n) acc += weight(x0 + e, x[e]);
+    return static_cast<double>(acc);
+  }
+  // first element of unit u whose running sum, after `run`, passes target
+  // (-1 if none); the last element of positive weight goes to *lastpos
+  __device__ int find(int u, double run, double target, int* lastpos) const {
+    using W = typename Terms<A, false, false>::W;
+    float x[E];
+    load(u, x);
+    const int n = count(u), x0 = first(u);
+    W acc = W(0);
+    int found = -1;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      if (e < n && found < 0) {
+        const W w = weight(x0 + e, x[e]);
+        acc += w;
+        if (w > W(0)) {
+          *lastpos = x0 + e;
+          if (run + static_cast<double>(acc) > target) found = x0 + e;
+        }
+      }
+    }
+    return found;
+  }
+};
+
+template <typename T, class A>
+__global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
+  __shared__ SampleSmem sm_;
+  __shared__ WgScratch ws_;
+  Lds<SampleSmem>& sm = lds_ref(sm_);
+  Lds<WgScratch>& ws = lds_ref(ws_);
+  const int tid = threadIdx.x;
+  const int n1 = S.num_nodes;
+  const int b = static_cast<int>(blockIdx.x / static_cast<unsigned>(n1));
+  const int j = static_cast<int>(blockIdx.x - static_cast<unsigned>(b) * n1);
+  const int32_t* par = S.parents + static_cast<size_t>(b) * n1;
+
+  // the tree's links (every row checks them) and this node's children in order
+  if (tid == 0) {
+    sm.nkids = 0;
+    sm.nremoved = 0;
+  }
+  __syncthreads();
+  int bad = 0;
+  for (int base = 0; base < n1; base += kNT) {
+    const int i = base + tid;
+    int p = -2;
+    if (i < n1) {
+      p = par[i];
+      if (i == 0 ? p != -1 : (p < 0 || p >= i)) bad = 1;
+    }
+    const bool kid = i < n1 && i > 0 && p == j;
+    const double inc = block_incl_scan(ws, kid ? 1.0 : 0.0);
+    const int before = sm.nkids;
+    if (kid) sm.kids[before + static_cast<int>(inc) - 1] = i;
+    __syncthreads();
+    if (tid == kNT - 1) sm.nkids = before + static_cast<int>(inc);
+    __syncthreads();
+  }
+  bad = __syncthreads_or(bad);
+  if (bad) {
+    if (j == 0 && tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_BAD_PARENT));
+    return;
+  }
+  const int nk = sm.nkids;
+  if (nk == 0) return;
+
+  // the row's frame (its maximum) and a check that it is finite
+  const T* row = static_cast<const T*>(S.draft) + (static_cast<size_t>(b) * n1 + j) *
+                                                      static_cast<size_t>(S.vocab);
+  const Geom geo = row_geom(row, S.vocab);
+  StripeResult st;
+  stripe_stats<T, A, false>(ws, row, row, geo, stripe(geo, 0, 1), ar, st);
+  if (!(st.m0 > -INFINITY) || !isfinite(st.s0)) {
+    if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_NONFINITE));
+    return;
+  }
+  const RowWeights<T, A> rw{row, geo, ar, ar.frame(st.m0), &sm};
+
+  // thread t owns the units [ub, ue): contiguous, so thread order is token order
+  const int U = rw.units();
+  const int ub = static_cast<int>(static_cast<long long>(U) * tid / kNT);
+  const int ue = static_cast<int>(static_cast<long long>(U) * (tid + 1) / kNT);
+  auto thread_sum = [&]() {
+    double acc = 0.0;
+#pragma unroll 4
+    for (int u = ub; u < ue; ++u) acc += rw.unit_sum(u);
+    return acc;
+  };
+  double ts = thread_sum();
+
+  for (int k = 0; k < nk; ++k) {
+    const int child = sm.kids[k];
+    const double incl = block_incl_scan(ws, ts);
+    if (tid == kNT - 1) sm.W = incl;
+    if (tid == 0) sm.owner = kNT;
+    __syncthreads();
+    const double W = sm.W;
+    if (!(W > 0.0)) {          // every token already drawn: not enough tokens for the siblings
+      if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_DEGENERATE));
+      return;
+    }
+    const double target =
+        static_cast<double>(S.uniforms[static_cast<size_t>(b) * n1 + child]) * W;
+    if (incl > target)
+      __hip_atomic_fetch_min(&sm.owner, tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __syncthreads();
+    const int owner = sm.owner;     // < kNT: the last thread's sum is W > target
+    if (tid == owner) {
+      double run = incl - ts;
+      int tok = -1, lastpos = -1;
+      for (int u = ub; u < ue && tok < 0; ++u) {
+        tok = rw.find(u, run, target, &lastpos);
+        if (tok < 0) run += rw.unit_sum(u);
+      }
+      if (tok < 0) tok = lastpos;   // rounding left no boundary past the target
+      sm.token = tok;
+      S.tokens[static_cast<size_t>(b) * n1 + child] = tok;
+      if (tok < 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_DEGENERATE));
+    }
+    __syncthreads();
+    if (sm.token < 0) return;
+    if (S.mode == TV_SIBLINGS_WITHOUT_REPLACEMENT && k + 1 < nk) {
+      if (tid == 0) sm.removed[sm.nremoved++] = sm.token;
+      __syncthreads();
+      if (tid == owner) ts = thread_sum();   // the drawn token lies in the owner's units
+      __syncthreads();
+    }
+  }
+}
+
+template <typename T, class A>
+int launch_sample_typed(const SampleParams& S, A ar, hipStream_t stream) {
+  const long long rows = static_cast<long long>(S.batch) * S.num_nodes;
+  hipLaunchKernelGGL(sample_init_kernel, dim3(static_cast<unsigned>((S.batch + 255) / 256)),
+                     dim3(256), 0, stream, S);
+  if (hipGetLastError() != hipSuccess) return TV_ERR_HIP;
+  hipLaunchKernelGGL((sample_kernel<T, A>), dim3(static_cast<unsigned>(rows)), dim3(kNT), 0,
+                     stream, S, ar);
+  if (hipGetLastError() != hipSuccess) return TV_ERR_HIP;
+  hipLaunchKernelGGL(sample_finish_kernel, dim3(static_cast<unsigned>((rows + 255) / 256)),
+                     dim3(256), 0, stream, S);
+  return hipGetLastError() == hipSuccess ? TV_OK : TV_ERR_HIP;
+}
+
 }  // namespace
 
 namespace tv {
@@ -2203,6 +2438,22 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
                  : launch_cap<uint16_t, kCapLarge>(P, precise, stream);
   return small ? launch_cap<float, kCapSmall>(P, true, stream)
                : launch_cap<float, kCapLarge>(P, true, stream);
+}
+
+}  // namespace tv
+
+namespace tv {
+
+int launch_sample(const SampleArgs& a, hipStream_t stream) {
+  SampleParams S{a.parents, a.draft, a.uniforms, a.tokens, a.status,
+                 a.batch, a.num_nodes, a.vocab, a.mode};
+  const double k64 = 1.4426950408889634 / static_cast<double>(a.temperature);
+  const bool precise = a.dtype == TV_DTYPE_F32 || a.vocab < kPreciseBelowVocab;
+  if (a.dtype == TV_DTYPE_BF16) {
+    if (!precise) return launch_sample_typed<uint16_t>(S, FastArith{static_cast<float>(k64)}, stream);
+    return launch_sample_typed<uint16_t>(S, PreciseArith{k64}, stream);
+  }
+  return launch_sample_typed<float>(S, PreciseArith{k64}, stream);
 }
 
 }  // namespace tv

@@ -73,6 +73,26 @@ inline WorkspaceLayout workspace_layout(int32_t batch, int32_t vocab) {
 // Argument checks that need no GPU. Returns a tv_status_t.
 int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes);
 
+struct SampleArgs {
+  int32_t batch;
+  int32_t num_nodes;
+  int32_t vocab;
+  const int32_t* parents;
+  const void* draft;
+  int32_t dtype;          // TV_DTYPE_*
+  float temperature;
+  const float* uniforms;
+  int32_t mode;           // TV_SIBLINGS_*
+  int32_t* tokens;
+  int32_t* status;
+};
+
+// Argument checks of the sampler that need no GPU. Returns a tv_status_t.
+int validate_sample(const SampleArgs& a);
+
+// Enqueue the draft-tree token sampler on `stream` (arguments validated).
+int launch_sample(const SampleArgs& a, hipStream_t stream);
+
 // Enqueue the verification on `stream` (an initialisation kernel, then the
 // cooperative verifier). Arguments already validated. Returns a tv_status_t.
 int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream);

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_function():
     lib = tv.load_library()
     names = declared_functions()
     assert {"tv_verify", "tv_verify_tokenlevel", "tv_workspace_size",
-            "tv_status_string"} <= set(names)
+            "tv_status_string", "tv_draft_tokens"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
 
@@ -140,3 +140,40 @@ def test_empty_batch_is_a_no_op(fn):
     assert call(fn, batch=0, parents=None, tokens=None, target_logits=None, draft_logits=None,
                 uniforms=None, accept_len=None, accepted_node=None, bonus_token=None,
                 status=None) == tv.TV_OK
+
+
+def call_sampler(**kw):
+    args = dict(batch=2, num_nodes=5, vocab=100, parents=A, draft_logits=A + 0x1000,
+                dtype=tv.TV_DTYPE_BF16, temperature=1.0, uniforms=A, mode=0, tokens=A, status=A)
+    args.update(kw)
+    return tv.tv_draft_tokens(**args)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(batch=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(num_nodes=0), tv.TV_ERR_INVALID_ARG),
+    (dict(vocab=1), tv.TV_ERR_INVALID_ARG),
+    (dict(dtype=7), tv.TV_ERR_INVALID_ARG),
+    (dict(mode=2), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=0.0), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=float("nan")), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=1e-5), tv.TV_ERR_UNSUPPORTED),
+    (dict(num_nodes=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(vocab=tv.TV_MAX_VOCAB + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(batch=tv.TV_MAX_BATCH + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(parents=None), tv.TV_ERR_INVALID_ARG),
+    (dict(draft_logits=None), tv.TV_ERR_INVALID_ARG),
+    (dict(uniforms=None), tv.TV_ERR_INVALID_ARG),
+    (dict(tokens=None), tv.TV_ERR_INVALID_ARG),
+    (dict(status=None), tv.TV_ERR_INVALID_ARG),
+    (dict(draft_logits=A + 1), tv.TV_ERR_INVALID_ARG),
+    (dict(tokens=A + 2), tv.TV_ERR_INVALID_ARG),
+])
+def test_sampler_argument_errors_launch_nothing(kw, want):
+    """Host-side validation of tv_draft_tokens returns before any HIP call (no GPU here)."""
+    assert call_sampler(**kw) == want
+
+
+def test_sampler_empty_batch_is_ok():
+    assert call_sampler(batch=0, parents=None, draft_logits=None, uniforms=None, tokens=None,
+                        status=None) == tv.TV_OK
