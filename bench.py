@@ -109,6 +109,60 @@ def cpu_baseline(batch, gpu_outs: dict, sample: int, workers: int):
     return sample / dt, dt, reps
 
 
+def sampler_leg(batch, steps: int, stream, elem: int) -> dict:
+    """Times tv_draft_tokens (the device draft-tree sampler) on the trees and
+    draft logits of one benchmark step with fresh uniforms per launch, and
+    checks 16 trees against the oracle. Algorithmic bytes: one read of the
+    draft row of every node that has children."""
+    import numpy as np
+    import torch
+
+    import paper_2505_12398_amd as tv
+    import workloads as W
+    from oracle import draft_sampler as DS
+    par = batch["parents"]
+    B, n1 = par.shape
+    V = batch["draft"].shape[-1]
+    par_h = par.cpu().numpy()
+    internal = sum(len(set(row[1:].tolist())) for row in par_h)
+    alg = internal * V * elem
+    times = []
+    for s in range(steps):
+        rng = np.random.default_rng(1000 + s)
+        u = torch.as_tensor(W.uniforms_np(rng, (B, n1)), device=par.device)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        ev0.record(stream)
+        tok, st = tv.draft_tokens(par, batch["draft"], batch["temperature"], u, batch["mode"],
+                                  stream=stream.cuda_stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        times.append(ev0.elapsed_time(ev1))
+    ms = sum(times) / len(times)
+    tok_h, st_h, u_h = tok.cpu().numpy(), st.cpu().numpy(), u.cpu().numpy()
+    exact = near = fail = 0
+    for b in range(0, B, max(1, B // 16)):
+        rows = batch["draft"][b].detach().cpu()
+        rows = rows.view(torch.int16).numpy().view(np.uint16) if rows.dtype == torch.bfloat16 \
+            else rows.numpy()
+        ref = DS.draw_tree_tokens(par_h[b], rows, batch["temperature"], u_h[b], batch["mode"])
+        if st_h[b] == ref.status and np.array_equal(tok_h[b], ref.tokens):
+            exact += 1
+        elif st_h[b] == ref.status and ref.margin < 1e-6:
+            near += 1
+        else:
+            fail += 1
+    gbps = alg / (ms * 1e-3) / 1e9
+    return {"ms_per_step": ms, "trees_per_s": B / (ms * 1e-3), "rows_with_children": internal,
+            "algorithmic_bytes_per_launch": alg, "achieved_GBps": gbps,
+            "frac": gbps / HBM_PEAK_GBPS, "bound": "hbm",
+            "kernel": "sample_kernel<uint16_t, FastArith> (tv_draft_tokens)",
+            "parity_sample": {"trees": exact + near + fail, "exact": exact, "near_ties": near,
+                              "failures": fail}}
+
+
 def _oracle_one(args):
     (par, tok, zb, zs, u), T, mode = args
     from oracle import verify_tree
@@ -126,6 +180,8 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=0)
     ap.add_argument("--mode", choices=["without", "with"], default="without")
     ap.add_argument("--tokenlevel-steps", type=int, default=20)
+    ap.add_argument("--sampler-steps", type=int, default=20,
+                    help="timed launches of the draft-tree token sampler on the same trees")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="only run plain device-to-device copies of this size (to scale "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -261,6 +317,9 @@ def main():
         res["accept_len_mean"]["delta_pct"] = 100.0 * (
             res["accept_len_mean"]["traversal_same_steps"] / res["accept_len_mean"]["tokenlevel"]
             - 1.0)
+
+    if args.sampler_steps > 0 and last is not None:
+        res["draft_sampler"] = sampler_leg(last[0], args.sampler_steps, stream, elem)
 
     if args.cpu_sample > 0 and last is not None:
         workers = args.cpu_workers or min(16, os.cpu_count() or 1)

@@ -2180,11 +2180,19 @@ struct SampleParams {
   int batch, num_nodes, vocab, mode;
 };
 
+constexpr int kSampleChunk = 64;        // units per chunk: one per lane of a wave
+// chunks of a row: at most 2^17 vectors plus 14 head and tail elements
+// (V <= 2^20 bf16 or 2^19 fp32), so 2049
+constexpr int kSampleMaxChunks = 2056;
+constexpr int kRowChunksInFlight = 8;      // chunks a wave loads before it sums them
+
 struct SampleSmem {
+  double cs[kSampleMaxChunks];     // chunk weight sums, in the row's frame once rescaled
+  float cm[kSampleMaxChunks];      // chunk maxima
   int32_t kids[TV_MAX_NODES];      // children of the row's node, ascending
   int32_t removed[TV_MAX_NODES];   // tokens drawn so far at this row (without replacement)
-  int nkids, nremoved, owner, token;
-  double W;
+  int nkids, nremoved, owner, chunk, token;
+  double W, run;
 };
 
 // Every tree starts OK with the root's token -1; the rows then raise status.
@@ -2203,18 +2211,19 @@ __global__ void __launch_bounds__(256) sample_finish_kernel(SampleParams S) {
   if (S.status[i / S.num_nodes] != TV_TREE_OK) S.tokens[i] = -1;
 }
 
-// The weights of one row are 2^(z*k + c) in the frame c of its maximum,
-// grouped in units: head elements (up to the first 16-byte boundary),
-// 16-byte vectors, tail elements, in token order. A unit's sum and the running
-// sum inside it are formed in the same order, so a rescan reproduces the sums
-// that chose it. Tokens already drawn (without replacement) weigh 0.
+// The weights of one row are 2^(z*k + c) in a frame c, grouped in units:
+// head elements (up to the first 16-byte boundary), 16-byte vectors, tail
+// elements, in token order; 64 consecutive units form a chunk. A unit's sum
+// and the running sum inside it are formed in the same order, so a rescan
+// reproduces the sum that chose it. Tokens already drawn (without
+// replacement) weigh 0.
 template <typename T, class A>
 struct RowWeights {
   static constexpr int E = Elem<T>::E;
+  using W = typename Terms<A, false, false>::W;
   const T* row;
   Geom g;
   A ar;
-  double c;
   const Lds<SampleSmem>* sm;
 
   __device__ int units() const { return g.head + g.nvec + g.tail; }
@@ -2234,30 +2243,38 @@ struct RowWeights {
       Elem<T>::unpack(load16(row, g.head, u - g.head), x);
     } else {
       x[0] = Elem<T>::scalar(row + first(u));
+#pragma unroll
+      for (int e = 1; e < E; ++e) x[e] = -INFINITY;
     }
   }
-  // weight of element e of unit u with value z
-  __device__ typename Terms<A, false, false>::W weight(int x, float z) const {
-    using W = typename Terms<A, false, false>::W;
+  __device__ float vmax(const float (&x)[E]) const {
+    float m = x[0];
+#pragma unroll
+    for (int e = 1; e < E; ++e) m = fmaxf(m, x[e]);
+    return m;
+  }
+  __device__ W weight(int x, float z, double c) const {
     if (sm->nremoved && drawn(x)) return W(0);
     if constexpr (A::kPrecise) return ar.ex(z, c);
     else return fast_exp2(fmaf(z, ar.k, static_cast<float>(c)));
   }
-  __device__ double unit_sum(int u) const {
-    using W = typename Terms<A, false, false>::W;
-    float x[E];
-    load(u, x);
+  // sum of unit u's weights in frame c, its values already loaded
+  __device__ double sum_of(int u, const float (&x)[E], double c) const {
     const int n = count(u), x0 = first(u);
     W acc = W(0);
 #pragma unroll
     for (int e = 0; e < E; ++e)
-      if (e < n) acc += weight(x0 + e, x[e]);
+      if (e < n) acc += weight(x0 + e, x[e], c);
     return static_cast<double>(acc);
+  }
+  __device__ double unit_sum(int u, double c) const {
+    float x[E];
+    load(u, x);
+    return sum_of(u, x, c);
   }
   // first element of unit u whose running sum, after `run`, passes target
   // (-1 if none); the last element of positive weight goes to *lastpos
-  __device__ int find(int u, double run, double target, int* lastpos) const {
-    using W = typename Terms<A, false, false>::W;
+  __device__ int find(int u, double c, double run, double target, int* lastpos) const {
     float x[E];
     load(u, x);
     const int n = count(u), x0 = first(u);
@@ -2266,7 +2283,7 @@ struct RowWeights {
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       if (e < n && found < 0) {
-        const W w = weight(x0 + e, x[e]);
+        const W w = weight(x0 + e, x[e], c);
         acc += w;
         if (w > W(0)) {
           *lastpos = x0 + e;
@@ -2284,7 +2301,7 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   __shared__ WgScratch ws_;
   Lds<SampleSmem>& sm = lds_ref(sm_);
   Lds<WgScratch>& ws = lds_ref(ws_);
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n1 = S.num_nodes;
   const int b = static_cast<int>(blockIdx.x / static_cast<unsigned>(n1));
   const int j = static_cast<int>(blockIdx.x - static_cast<unsigned>(b) * n1);
@@ -2320,29 +2337,76 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   const int nk = sm.nkids;
   if (nk == 0) return;
 
-  // the row's frame (its maximum) and a check that it is finite
   const T* row = static_cast<const T*>(S.draft) + (static_cast<size_t>(b) * n1 + j) *
                                                       static_cast<size_t>(S.vocab);
-  const Geom geo = row_geom(row, S.vocab);
-  StripeResult st;
-  stripe_stats<T, A, false>(ws, row, row, geo, stripe(geo, 0, 1), ar, st);
-  if (!(st.m0 > -INFINITY) || !isfinite(st.s0)) {
+  const RowWeights<T, A> rw{row, row_geom(row, S.vocab), ar, &sm};
+  const int U = rw.units();
+  const int C = (U + kSampleChunk - 1) / kSampleChunk;
+  if (C > kSampleMaxChunks) {      // beyond the vocabulary limits the host checks
+    if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_DEGENERATE));
+    return;
+  }
+
+  // One read of the row: wave w sums chunks w, w + 4, ..., each in the frame
+  // of its own maximum, with kRowChunksInFlight chunks' loads issued together.
+  float wmax = -INFINITY;
+  for (int c0 = wave; c0 < C; c0 += kNW * kRowChunksInFlight) {
+    float x[kRowChunksInFlight][RowWeights<T, A>::E];
+    int uu[kRowChunksInFlight];
+#pragma unroll
+    for (int i = 0; i < kRowChunksInFlight; ++i) {
+      const int c = c0 + i * kNW;
+      const int u = c * kSampleChunk + lane;
+      uu[i] = u < U ? u : U - 1;                  // clamped: the load is always in the row
+      rw.load(uu[i], x[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < kRowChunksInFlight; ++i) {
+      const int c = c0 + i * kNW;
+      if (c >= C) break;
+      const bool in = c * kSampleChunk + lane < U;
+      const float M = wave_max(in ? rw.vmax(x[i]) : -INFINITY);
+      double us = 0.0;
+      if (in) us = (M > -INFINITY) ? rw.sum_of(uu[i], x[i], ar.frame(M))
+                                   : rw.sum_of(uu[i], x[i], 0.0);   // 0, or NaN for a NaN
+      const double sum = wave_sum(us);
+      if (lane == 0) {
+        sm.cs[c] = sum;
+        sm.cm[c] = M;
+      }
+      wmax = fmaxf(wmax, M);
+    }
+  }
+  if (lane == 0) ws.red_f[wave] = wmax;
+  __syncthreads();
+  float rowmax = ws.red_f[0];
+#pragma unroll
+  for (int w = 1; w < kNW; ++w) rowmax = fmaxf(rowmax, ws.red_f[w]);
+  __syncthreads();
+  if (!(rowmax > -INFINITY) || rowmax == INFINITY) {
     if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_NONFINITE));
     return;
   }
-  const RowWeights<T, A> rw{row, geo, ar, ar.frame(st.m0), &sm};
+  const double cf = ar.frame(rowmax);   // the row's frame
 
-  // thread t owns the units [ub, ue): contiguous, so thread order is token order
-  const int U = rw.units();
-  const int ub = static_cast<int>(static_cast<long long>(U) * tid / kNT);
-  const int ue = static_cast<int>(static_cast<long long>(U) * (tid + 1) / kNT);
-  auto thread_sum = [&]() {
-    double acc = 0.0;
-#pragma unroll 4
-    for (int u = ub; u < ue; ++u) acc += rw.unit_sum(u);
-    return acc;
-  };
-  double ts = thread_sum();
+  // chunk sums into the row's frame; thread t owns the chunks [cb, ce)
+  const int cb = static_cast<int>(static_cast<long long>(C) * tid / kNT);
+  const int ce = static_cast<int>(static_cast<long long>(C) * (tid + 1) / kNT);
+  double ts = 0.0;
+  int nonfinite = 0;
+  for (int c = cb; c < ce; ++c) {
+    const float M = sm.cm[c];
+    double v = sm.cs[c];
+    if (M > -INFINITY) v *= exp2(cf - ar.frame(M));
+    if (!isfinite(v)) nonfinite = 1;
+    sm.cs[c] = v;
+    ts += v;
+  }
+  nonfinite = __syncthreads_or(nonfinite);
+  if (nonfinite) {
+    if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_NONFINITE));
+    return;
+  }
 
   for (int k = 0; k < nk; ++k) {
     const int child = sm.kids[k];
@@ -2362,23 +2426,81 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
     __syncthreads();
     const int owner = sm.owner;     // < kNT: the last thread's sum is W > target
     if (tid == owner) {
+      // the owner's chunk holding the target (else its last chunk of positive weight)
       double run = incl - ts;
-      int tok = -1, lastpos = -1;
-      for (int u = ub; u < ue && tok < 0; ++u) {
-        tok = rw.find(u, run, target, &lastpos);
-        if (tok < 0) run += rw.unit_sum(u);
+      int hit = -1, lastc = -1;
+      for (int c = cb; c < ce && hit < 0; ++c) {
+        if (sm.cs[c] > 0.0) lastc = c;
+        if (sm.cs[c] > 0.0 && run + sm.cs[c] > target) hit = c;
+        else run += sm.cs[c];
       }
-      if (tok < 0) tok = lastpos;   // rounding left no boundary past the target
-      sm.token = tok;
-      S.tokens[static_cast<size_t>(b) * n1 + child] = tok;
-      if (tok < 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_DEGENERATE));
+      if (hit < 0) {
+        hit = lastc;
+        run = -INFINITY;            // take its last token of positive weight
+      }
+      sm.chunk = hit;
+      sm.run = run;
     }
     __syncthreads();
-    if (sm.token < 0) return;
+    if (tid < 64) {
+      // wave 0 rescans the chunk, one unit per lane, in the row's frame
+      const int c = sm.chunk;
+      int tok = -1;
+      if (c >= 0) {
+        const int u = c * kSampleChunk + lane;
+        const double us = u < U ? rw.unit_sum(u, cf) : 0.0;
+        double inc = us;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const double o = __shfl_up(inc, off, 64);
+          if (lane >= off) inc += o;
+        }
+        const double run = sm.run;
+        const uint64_t pos = __ballot(us > 0.0);
+        const uint64_t hitm = __ballot(u < U && us > 0.0 && run + inc > target);
+        const int L = hitm ? __ffsll(static_cast<unsigned long long>(hitm)) - 1
+                           : (pos ? 63 - __clzll(static_cast<long long>(pos)) : -1);
+        int t = -1, lp = -1;
+        if (L >= 0 && lane == L) {
+          t = rw.find(u, cf, hitm ? run + (inc - us) : -INFINITY, target, &lp);
+          if (t < 0) t = lp;        // rounding left the boundary just short of the unit's end
+        }
+        if (L >= 0) tok = __shfl(t, L, 64);
+      }
+      if (lane == 0) {
+        sm.token = tok;
+        S.tokens[static_cast<size_t>(b) * n1 + child] = tok;
+        if (tok < 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_DEGENERATE));
+      }
+    }
+    __syncthreads();
+    const int tok = sm.token;
+    if (tok < 0) return;
     if (S.mode == TV_SIBLINGS_WITHOUT_REPLACEMENT && k + 1 < nk) {
-      if (tid == 0) sm.removed[sm.nremoved++] = sm.token;
+      // the token leaves its chunk's sum and the owning thread's
+      const int u = tok < rw.g.head ? tok
+                    : (tok < rw.g.head + rw.g.nvec * RowWeights<T, A>::E
+                           ? rw.g.head + (tok - rw.g.head) / RowWeights<T, A>::E
+                           : rw.g.head + rw.g.nvec + (tok - rw.g.head - rw.g.nvec * RowWeights<T, A>::E));
+      const int c = u / kSampleChunk;
+      if (tid == 0) {
+        float x[RowWeights<T, A>::E];
+        rw.load(u, x);
+        const int e = tok - rw.first(u);
+        float z = x[0];
+#pragma unroll
+        for (int i = 1; i < RowWeights<T, A>::E; ++i)
+          if (i == e) z = x[i];
+        const double w = static_cast<double>(rw.weight(tok, z, cf));
+        const double v = sm.cs[c] - w;
+        sm.cs[c] = v > 0.0 ? v : 0.0;
+        sm.removed[sm.nremoved++] = tok;
+      }
       __syncthreads();
-      if (tid == owner) ts = thread_sum();   // the drawn token lies in the owner's units
+      if (c >= cb && c < ce) {
+        ts = 0.0;
+        for (int cc = cb; cc < ce; ++cc) ts += sm.cs[cc];
+      }
       __syncthreads();
     }
   }
