@@ -2347,8 +2347,12 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
     return;
   }
 
-  // One read of the row: wave w sums chunks w, w + 4, ..., each in the frame
-  // of its own maximum, with kRowChunksInFlight chunks' loads issued together.
+  // One read of the row: wave w sums chunks w, w + 4, ..., with
+  // kRowChunksInFlight chunks' loads issued together; the chunks of one such
+  // round share the frame of their maximum. Chunk sums are fp32 on the fast
+  // path (a chunk is under 1% of a row's weight at the vocabularies it
+  // serves, so its rounding moves a chunk boundary by far less than the
+  // near-tie band) and fp64 on the precise one.
   float wmax = -INFINITY;
   for (int c0 = wave; c0 < C; c0 += kNW * kRowChunksInFlight) {
     float x[kRowChunksInFlight][RowWeights<T, A>::E];
@@ -2358,24 +2362,58 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
       const int c = c0 + i * kNW;
       const int u = c * kSampleChunk + lane;
       uu[i] = u < U ? u : U - 1;                  // clamped: the load is always in the row
-      rw.load(uu[i], x[i]);
     }
+    if (rw.g.nvec > 0) {
+      // every lane loads a 16-byte vector of the row (index clamped into the
+      // vectors) before anything is used, so all the round's loads are in
+      // flight together; lanes whose unit is a head or tail element then
+      // replace it with that element
+      uint4 raw[kRowChunksInFlight];
+#pragma unroll
+      for (int i = 0; i < kRowChunksInFlight; ++i) {
+        const int v = min(max(uu[i] - rw.g.head, 0), rw.g.nvec - 1);
+        raw[i] = load16(row, rw.g.head, v);
+      }
+#pragma unroll
+      for (int i = 0; i < kRowChunksInFlight; ++i) pin(raw[i]);
+#pragma unroll
+      for (int i = 0; i < kRowChunksInFlight; ++i) {
+        Elem<T>::unpack(raw[i], x[i]);
+        if (rw.count(uu[i]) != RowWeights<T, A>::E) rw.load(uu[i], x[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kRowChunksInFlight; ++i) rw.load(uu[i], x[i]);
+    }
+    float lm = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kRowChunksInFlight; ++i) {
+      const int c = c0 + i * kNW;
+      if (c < C && c * kSampleChunk + lane < U) lm = fmaxf(lm, rw.vmax(x[i]));
+    }
+    const float M = wave_max(lm);
+    const double fr = (M > -INFINITY) ? ar.frame(M) : 0.0;   // all -inf: weights 0 (or NaN)
 #pragma unroll
     for (int i = 0; i < kRowChunksInFlight; ++i) {
       const int c = c0 + i * kNW;
       if (c >= C) break;
       const bool in = c * kSampleChunk + lane < U;
-      const float M = wave_max(in ? rw.vmax(x[i]) : -INFINITY);
-      double us = 0.0;
-      if (in) us = (M > -INFINITY) ? rw.sum_of(uu[i], x[i], ar.frame(M))
-                                   : rw.sum_of(uu[i], x[i], 0.0);   // 0, or NaN for a NaN
-      const double sum = wave_sum(us);
+      const double us = in ? rw.sum_of(uu[i], x[i], fr) : 0.0;
+      double sum;
+      if constexpr (A::kPrecise) {
+        sum = wave_sum(us);
+      } else {
+        float v = static_cast<float>(us);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+        sum = static_cast<double>(v);
+      }
       if (lane == 0) {
         sm.cs[c] = sum;
         sm.cm[c] = M;
       }
-      wmax = fmaxf(wmax, M);
     }
+    wmax = fmaxf(wmax, M);
   }
   if (lane == 0) ws.red_f[wave] = wmax;
   __syncthreads();
