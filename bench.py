@@ -109,6 +109,53 @@ def cpu_baseline(batch, gpu_outs: dict, sample: int, workers: int):
     return sample / dt, dt, reps
 
 
+def deep_leg(steps: int, mode: int, stream, elem: int, V: int) -> dict:
+    """tv_verify (no theta: early rejection) on Sequoia-scale trees: 8 trees of
+    767 draft nodes (depth about 30), V=128256 bf16, fresh seeds per launch,
+    with the oracle on one tree of the last launch."""
+    import numpy as np
+    import torch
+
+    import paper_2505_12398_amd as tv
+    import workloads as W
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity  # noqa: E402  (test infrastructure: oracle comparison)
+    times, nbytes, acc = [], [], []
+    out = batch = None
+    for s in range(steps + 2):
+        batch = W.make_deep_batch(step=s, device=torch.device("cuda", 0), mode=mode, vocab=V)
+        B, n1 = batch["parents"].shape
+        ws, _ = tv.workspace_tensor(B, n1, V, batch["target"].device)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        ev0.record(stream)
+        out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"], batch["draft"],
+                              batch["temperature"], batch["uniforms"], mode, want_nodes=False,
+                              want_counters=True, stream=stream.cuda_stream, workspace=ws)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        if s >= 2:                     # two untimed warmup launches
+            times.append(ev0.elapsed_time(ev1))
+            nbytes.append(algorithmic_bytes(out.counters, V, elem, n1)["total"])
+            acc.append(out.accept_len.float().mean().item() + 1.0)
+    ms = sum(times) / len(times)
+    alg = sum(nbytes) / len(nbytes)
+    gpu = parity.host_outputs(tv.verify_batch(
+        batch["parents"], batch["tokens"], batch["target"], batch["draft"],
+        batch["temperature"], batch["uniforms"], mode, want_nodes=True, want_theta=False))
+    kind, msg, _ = parity.compare_tree(gpu, 0, parity.oracle_tree(batch, 0, False), False, False,
+                                       "bf16")
+    B, n1 = batch["parents"].shape
+    depth = max(int(W.node_depths(p).max()) for p in batch["parents"].cpu().numpy())
+    return {"workload": W.DEEP_NAME, "trees": B, "nodes_per_tree": n1, "max_depth": depth,
+            "ms_per_step": ms, "trees_per_s": B / (ms * 1e-3),
+            "algorithmic_bytes_per_launch": alg, "achieved_GBps": alg / (ms * 1e-3) / 1e9,
+            "frac": alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, "accept_len_mean": sum(acc) / len(acc),
+            "parity_tree0": kind if kind != "fail" else f"fail: {msg}"}
+
+
 def sampler_leg(batch, steps: int, stream, elem: int) -> dict:
     """Times tv_draft_tokens (the device draft-tree sampler) on the trees and
     draft logits of one benchmark step with fresh uniforms per launch, and
@@ -180,6 +227,8 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=0)
     ap.add_argument("--mode", choices=["without", "with"], default="without")
     ap.add_argument("--tokenlevel-steps", type=int, default=20)
+    ap.add_argument("--deep-steps", type=int, default=8,
+                    help="timed launches on Sequoia-scale trees (8 trees x 768 nodes, V=128256)")
     ap.add_argument("--sampler-steps", type=int, default=20,
                     help="timed launches of the draft-tree token sampler on the same trees")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
@@ -317,6 +366,9 @@ def main():
         res["accept_len_mean"]["delta_pct"] = 100.0 * (
             res["accept_len_mean"]["traversal_same_steps"] / res["accept_len_mean"]["tokenlevel"]
             - 1.0)
+
+    if args.deep_steps > 0:
+        res["deep_trees"] = deep_leg(args.deep_steps, mode, stream, elem, V)
 
     if args.sampler_steps > 0 and last is not None:
         res["draft_sampler"] = sampler_leg(last[0], args.sampler_steps, stream, elem)

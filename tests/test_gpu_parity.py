@@ -215,6 +215,19 @@ def test_large_trees():
             assert_clean(rep, "1024-node trees, early rejection")
 
 
+@pytest.mark.parametrize("mode", MODES)
+def test_deep_trees(mode):
+    """Sequoia-scale trees (767 draft nodes, depth about 30, hundreds of
+    internal nodes) with the large-batch logit law at a reduced vocabulary
+    (V = 4099, fp32): every tree, both verifiers, with and without theta."""
+    bt = W.make_deep_batch(batch=4, vocab=4099, step=1, device=DEV, mode=mode, dtype="f32")
+    for tl in (False, True):
+        rep = parity.check(bt, tl, label=f"deep mode={mode} tl={tl}")
+        assert_clean(rep, f"deep trees mode={mode} tokenlevel={tl}")
+    rep = parity.check(bt, False, label=f"deep-early mode={mode}", theta=False)
+    assert_clean(rep, f"deep trees mode={mode} early rejection")
+
+
 def test_identical_models_accept_first_leaf():
     rng = np.random.default_rng(3)
     par = np.tile(W.binary_parents(3), (8, 1))

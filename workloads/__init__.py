@@ -317,6 +317,52 @@ def draw_tokens(parents: np.ndarray, draft, temperature: float, mode: int, seed:
     return tokens
 
 
+def windowed_parents(rng: np.random.Generator, n_nodes: int, window: int) -> np.ndarray:
+    """Random recursive tree of ``n_nodes`` draft nodes: node i's parent is
+    uniform over the ``window`` nodes before it (all earlier nodes while
+    i <= window), so depth grows about as 2N / window and nodes have a few
+    children each."""
+    parents = np.empty(n_nodes + 1, dtype=np.int32)
+    parents[0] = -1
+    for i in range(1, n_nodes + 1):
+        parents[i] = rng.integers(max(0, i - window), i)
+    return parents
+
+
+DEEP_NAME = "deep-N767-w64-B8-V128256"
+
+
+def make_deep_batch(batch: int = 8, n_nodes: int = 767, window: int = 64, vocab: int = 128256,
+                    step: int = 0, device="cpu", mode: int = WITHOUT_REPLACEMENT, seed: int = 0,
+                    dtype: str = "bf16"):
+    """Large, deep trees at the scale of the paper's Sequoia comparison
+    (hundreds of nodes, depth above 20): ``windowed_parents`` trees with the
+    large-batch workload's logit law (target N(0, 3^2) plus the sparse +6
+    boosts, draft = target + N(0, 1.5^2), T = 1), tokens drawn from the
+    parent's draft in the given sibling mode, uniforms k * 2^-24."""
+    import torch
+    cfg = CONFIGS[5]
+    keys = (seed, 99, step)
+    parents = np.empty((batch, n_nodes + 1), dtype=np.int32)
+    for b in range(batch):
+        rng = np.random.default_rng(np.random.SeedSequence(list(keys) + [1, b]))
+        parents[b] = windowed_parents(rng, n_nodes, window)
+    zb, zs = make_logits(cfg, parents, vocab, _seed(*keys, 2), device)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    zb = zb.to(tdt)
+    zs = zs.to(tdt)
+    tokens = draw_tokens(parents, zs, cfg.temperature, mode, _seed(*keys, 3), chunk=2)
+    g = torch.Generator(device=device)
+    g.manual_seed(_seed(*keys, 4))
+    u = torch.randint(0, 2 ** 24, parents.shape, generator=g, device=device).to(torch.float32)
+    u.mul_(U_SCALE)
+    return {
+        "config": cfg, "parents": torch.as_tensor(parents, device=device),
+        "tokens": tokens, "target": zb, "draft": zs, "uniforms": u,
+        "temperature": cfg.temperature, "mode": mode, "dtype": dtype,
+    }
+
+
 def make_batch(cfg_id: int, step: int = 0, device="cpu", mode: int = WITHOUT_REPLACEMENT,
                batch: int | None = None, vocab: int | None = None, seed: int = 0):
     """One batch of a config: dict with parents, tokens, target, draft (dtype of
