@@ -465,6 +465,24 @@ def verify_tree_tokenlevel(parents, tokens, target_logits, draft_logits, tempera
 
 
 # ---------------------------------------------------------------------------
+# The accepted output (Def. def2): the chain X^tau from the root, then Y
+# ---------------------------------------------------------------------------
+
+def committed_sequence(parents, tokens, accepted_node: int, bonus_token: int):
+    """The verification output as it is committed for the next cycle: the
+    nodes of the accepted chain X^tau after the root, in order from the root
+    (the drafted positions whose cache entries are kept), and their tokens
+    followed by Y. Returns (nodes, tokens), both lists."""
+    chain = []
+    x = int(accepted_node)
+    while x > 0:
+        chain.append(x)
+        x = int(parents[x])
+    chain.reverse()
+    return chain, [int(tokens[c]) for c in chain] + [int(bonus_token)]
+
+
+# ---------------------------------------------------------------------------
 # Algorithmic bytes (what any implementation of the method must move)
 # ---------------------------------------------------------------------------
 

@@ -422,11 +422,33 @@ def pin_draft_sampler_statuses():
     assert r.status == O.TREE_OK and sorted(r.tokens[1:3]) == [0, 1]
 
 
+def pin_committed_sequence():
+    """Def. def2 on the Sec. 3.2 tree (X1..X5 drafted tokens a, c, b, c, a):
+    accepting X4 outputs the chain X1 X4, tokens a c, then Y; accepting X2
+    outputs c then Y; accepting the root outputs Y alone. The chain has as many
+    nodes as the accepted node's depth."""
+    g = golden("worked_example.json")
+    par = g["parents"]
+    voc = {t: i for i, t in enumerate(g["vocab"])}
+    tok = [-1] + [voc[t] for t in g["tokens_X1_to_X5"]]
+    assert O.committed_sequence(par, tok, 4, 2) == ([1, 4], [voc["a"], voc["c"], 2])
+    assert O.committed_sequence(par, tok, 2, 0) == ([2], [voc["c"], 0])
+    assert O.committed_sequence(par, tok, 0, 1) == ([], [1])
+    rng = np.random.default_rng(5)
+    for _ in range(50):
+        p = W.geometric_bfs_parents(rng, 20, 5)
+        a = int(rng.integers(0, len(p)))
+        nodes, toks = O.committed_sequence(p, np.arange(len(p)), a, 7)
+        assert len(nodes) == W.node_depths(p)[a] and toks[-1] == 7
+        assert all(int(p[nodes[i + 1]]) == nodes[i] for i in range(len(nodes) - 1))
+        assert not nodes or int(p[nodes[0]]) == 0
+
+
 FAST_PINS = [pin_worked_example_trace, pin_worked_example_tokenlevel, pin_worked_example_law,
              pin_single_token_table1, pin_rrsw_example, pin_tempered_softmax_inverse,
              pin_inverse_cdf_law, pin_identical_models, pin_depth1_equals_rrsw,
              pin_invariants, pin_early_rejection_worked_example, pin_early_rejection_sound,
-             pin_draft_sampler_law, pin_draft_sampler_statuses]
+             pin_draft_sampler_law, pin_draft_sampler_statuses, pin_committed_sequence]
 ENUM_PINS = [pin_lossless_exact, pin_lossless_irregular_T07, pin_chain_optimality]
 ALL_PINS = FAST_PINS + ENUM_PINS
 
