@@ -109,6 +109,42 @@ def cpu_baseline(batch, gpu_outs: dict, sample: int, workers: int):
     return sample / dt, dt, reps
 
 
+def commit_leg(last, stream, steps: int = 20) -> dict:
+    """Times tv_commit_paths (the accepted-path commit) on the outputs of the
+    last timed verification and checks every tree against the oracle's
+    committed sequence."""
+    import numpy as np
+    import torch
+
+    import paper_2505_12398_amd as tv
+    from oracle import tv_oracle as O
+    batch, out = last
+    B, n1 = batch["parents"].shape
+    max_len = 16
+    times = []
+    for _ in range(steps):
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        ev0.record(stream)
+        pn, pt, pl = tv.commit_paths(batch["parents"], batch["tokens"], out, max_len,
+                                     stream=stream.cuda_stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        times.append(ev0.elapsed_time(ev1))
+    par, tok = batch["parents"].cpu().numpy(), batch["tokens"].cpu().numpy()
+    acc, y = out.accepted_node.cpu().numpy(), out.bonus_token.cpu().numpy()
+    pt_h, pl_h = pt.cpu().numpy(), pl.cpu().numpy()
+    exact = 0
+    for b in range(B):
+        _, toks = O.committed_sequence(par[b], tok[b], int(acc[b]), int(y[b]))
+        exact += int(pl_h[b] == len(toks) and list(pt_h[b, :len(toks)]) == toks)
+    return {"us_per_step": 1000.0 * sum(times) / len(times), "trees": B, "max_len": max_len,
+            "bound": "launch latency (a few bytes per tree)",
+            "parity": {"trees": B, "exact": exact}}
+
+
 def deep_leg(steps: int, mode: int, stream, elem: int, V: int) -> dict:
     """tv_verify (no theta: early rejection) on Sequoia-scale trees: 8 trees of
     767 draft nodes (depth about 30), V=128256 bf16, fresh seeds per launch,
@@ -366,6 +402,9 @@ def main():
         res["accept_len_mean"]["delta_pct"] = 100.0 * (
             res["accept_len_mean"]["traversal_same_steps"] / res["accept_len_mean"]["tokenlevel"]
             - 1.0)
+
+    if last is not None:
+        res["commit_paths"] = commit_leg(last, stream)
 
     if args.deep_steps > 0:
         res["deep_trees"] = deep_leg(args.deep_steps, mode, stream, elem, V)

@@ -233,6 +233,33 @@ int tv_draft_tokens(int32_t batch, int32_t num_nodes, int32_t vocab, const int32
                     const float* uniforms, int32_t mode, int32_t* tokens, int32_t* status,
                     hipStream_t stream);
 
+/* path_len codes of tv_commit_paths besides a length */
+#define TV_COMMIT_OVERFLOW (-1)       /* the chain is longer than max_len */
+#define TV_COMMIT_INCONSISTENT (-2)   /* accepted_node out of range or a link not pointing back */
+
+/*
+ * Accepted-path commit: the step after verification. For every tree, the
+ * output of Def. def2 (Sec. 3.3), the accepted chain X^tau and the token Y,
+ * laid out for the next decoding cycle:
+ *   path_nodes  int32 [batch][max_len]      nodes of X^tau after the root, from the root
+ *                                           down (the drafted positions whose cache
+ *                                           entries are kept), then -1
+ *   path_tokens int32 [batch][max_len + 1]  their drafted tokens, then Y, then -1
+ *   path_len    int32 [batch]               tokens committed, tau + 1; 0 for a tree whose
+ *                                           status is not TV_TREE_OK; TV_COMMIT_OVERFLOW or
+ *                                           TV_COMMIT_INCONSISTENT (rows then all -1)
+ * Inputs (device): parents and tokens as for tv_verify; accepted_node,
+ * bonus_token and status as tv_verify or tv_verify_tokenlevel wrote them.
+ * max_len in 0 .. TV_MAX_NODES (path_nodes may be NULL when it is 0). No
+ * workspace; nothing is allocated. Returns a tv_status_t; argument errors
+ * launch nothing.
+ */
+int tv_commit_paths(int32_t batch, int32_t num_nodes, const int32_t* parents,
+                    const int32_t* tokens, const int32_t* accepted_node,
+                    const int32_t* bonus_token, const int32_t* status, int32_t max_len,
+                    int32_t* path_nodes, int32_t* path_tokens, int32_t* path_len,
+                    hipStream_t stream);
+
 /* Static, human-readable name of a tv_status_t value ("unknown status" otherwise). */
 const char* tv_status_string(int code);
 

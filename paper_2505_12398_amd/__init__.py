@@ -17,6 +17,6 @@ from ._lib import (  # noqa: F401
     TV_MAX_BATCH, TV_MAX_NODES, TV_MAX_VOCAB, TV_MAX_VOCAB_F32, TV_NUM_COUNTERS,
     LIB_PATH, TvError, load_library,
     tv_workspace_size, tv_verify, tv_verify_tokenlevel, tv_status_string, tv_draft_tokens,
-    draft_tokens,
+    draft_tokens, tv_commit_paths, commit_paths, TV_COMMIT_OVERFLOW, TV_COMMIT_INCONSISTENT,
     VerifyOutputs, verify_batch, workspace_tensor,
 )

@@ -64,6 +64,9 @@ def load_library(path: str = LIB_PATH):
             fn.restype = ctypes.c_int
         lib.tv_draft_tokens.argtypes = _SAMPLE_ARGTYPES
         lib.tv_draft_tokens.restype = ctypes.c_int
+        lib.tv_commit_paths.argtypes = [ctypes.c_int32, ctypes.c_int32] + \
+            [ctypes.c_void_p] * 5 + [ctypes.c_int32] + [ctypes.c_void_p] * 4
+        lib.tv_commit_paths.restype = ctypes.c_int
         lib.tv_status_string.argtypes = [ctypes.c_int]
         lib.tv_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -162,6 +165,38 @@ def draft_tokens(parents, draft_logits, temperature, uniforms, mode, stream=None
     if st != TV_OK:
         raise TvError(st, "tv_draft_tokens")
     return tokens, status
+
+
+TV_COMMIT_OVERFLOW, TV_COMMIT_INCONSISTENT = -1, -2
+
+
+def tv_commit_paths(batch, num_nodes, parents, tokens, accepted_node, bonus_token, status,
+                    max_len, path_nodes, path_tokens, path_len, stream=None) -> int:
+    """C-ABI ``tv_commit_paths``: pointers may be torch tensors or raw ints;
+    returns the status."""
+    return int(load_library().tv_commit_paths(
+        int(batch), int(num_nodes), _ptr(parents), _ptr(tokens), _ptr(accepted_node),
+        _ptr(bonus_token), _ptr(status), int(max_len), _ptr(path_nodes), _ptr(path_tokens),
+        _ptr(path_len), _ptr(stream)))
+
+
+def commit_paths(parents, tokens, out: "VerifyOutputs", max_len: int, stream=None):
+    """The committed chain of every tree after a verification (torch tensors
+    in; (path_nodes, path_tokens, path_len) int32 tensors out); raises on a
+    non-OK return."""
+    import torch
+    B, n1 = parents.shape
+    dev = parents.device
+    pn = torch.empty((B, max(max_len, 1)), dtype=torch.int32, device=dev)
+    pt = torch.empty((B, max_len + 1), dtype=torch.int32, device=dev)
+    pl = torch.empty(B, dtype=torch.int32, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream if dev.type == "cuda" else None
+    st = tv_commit_paths(B, n1, parents, tokens, out.accepted_node, out.bonus_token, out.status,
+                         max_len, pn, pt, pl, stream)
+    if st != TV_OK:
+        raise TvError(st, "tv_commit_paths")
+    return pn[:, :max_len], pt, pl
 
 
 def workspace_tensor(batch: int, num_nodes: int, vocab: int, device):

@@ -130,6 +130,26 @@ int tv_draft_tokens(int32_t batch, int32_t num_nodes, int32_t vocab, const int32
   return tv::launch_sample(a, stream);
 }
 
+int tv_commit_paths(int32_t batch, int32_t num_nodes, const int32_t* parents,
+                    const int32_t* tokens, const int32_t* accepted_node,
+                    const int32_t* bonus_token, const int32_t* status, int32_t max_len,
+                    int32_t* path_nodes, int32_t* path_tokens, int32_t* path_len,
+                    hipStream_t stream) {
+  if (batch < 0 || num_nodes < 1 || max_len < 0) return TV_ERR_INVALID_ARG;
+  if (batch > TV_MAX_BATCH || num_nodes > TV_MAX_NODES || max_len > TV_MAX_NODES)
+    return TV_ERR_UNSUPPORTED;
+  if (batch == 0) return TV_OK;
+  const void* ptrs[] = {parents, tokens, accepted_node, bonus_token, status, path_tokens,
+                        path_len};
+  for (const void* p : ptrs)
+    if (!p || reinterpret_cast<uintptr_t>(p) % 4) return TV_ERR_INVALID_ARG;
+  if ((max_len > 0 && !path_nodes) || reinterpret_cast<uintptr_t>(path_nodes) % 4)
+    return TV_ERR_INVALID_ARG;
+  const tv::CommitArgs a{batch, num_nodes, parents, tokens, accepted_node, bonus_token, status,
+                         max_len, path_nodes, path_tokens, path_len};
+  return tv::launch_commit(a, stream);
+}
+
 const char* tv_status_string(int code) {
   switch (code) {
     case TV_OK: return "ok";

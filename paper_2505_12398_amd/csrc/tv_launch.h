@@ -87,6 +87,23 @@ struct SampleArgs {
   int32_t* status;
 };
 
+struct CommitArgs {
+  int32_t batch;
+  int32_t num_nodes;
+  const int32_t* parents;
+  const int32_t* tokens;
+  const int32_t* accepted_node;
+  const int32_t* bonus_token;
+  const int32_t* status;
+  int32_t max_len;
+  int32_t* path_nodes;
+  int32_t* path_tokens;
+  int32_t* path_len;
+};
+
+// Enqueue the accepted-path commit on `stream` (arguments validated).
+int launch_commit(const CommitArgs& a, hipStream_t stream);
+
 // Argument checks of the sampler that need no GPU. Returns a tv_status_t.
 int validate_sample(const SampleArgs& a);
 

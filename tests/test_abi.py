@@ -177,3 +177,31 @@ def test_sampler_argument_errors_launch_nothing(kw, want):
 def test_sampler_empty_batch_is_ok():
     assert call_sampler(batch=0, parents=None, draft_logits=None, uniforms=None, tokens=None,
                         status=None) == tv.TV_OK
+
+
+def call_commit(**kw):
+    args = dict(batch=2, num_nodes=5, parents=A, tokens=A, accepted_node=A, bonus_token=A,
+                status=A, max_len=4, path_nodes=A, path_tokens=A, path_len=A)
+    args.update(kw)
+    return tv.tv_commit_paths(**args)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(batch=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(num_nodes=0), tv.TV_ERR_INVALID_ARG),
+    (dict(max_len=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(num_nodes=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(max_len=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(parents=None), tv.TV_ERR_INVALID_ARG),
+    (dict(accepted_node=None), tv.TV_ERR_INVALID_ARG),
+    (dict(path_tokens=None), tv.TV_ERR_INVALID_ARG),
+    (dict(path_nodes=None), tv.TV_ERR_INVALID_ARG),
+    (dict(path_len=A + 2), tv.TV_ERR_INVALID_ARG),
+])
+def test_commit_argument_errors_launch_nothing(kw, want):
+    """Host-side validation of tv_commit_paths returns before any HIP call (no GPU here)."""
+    assert call_commit(**kw) == want
+
+
+def test_commit_empty_batch_is_ok():
+    assert call_commit(batch=0, parents=None, tokens=None) == tv.TV_OK
