@@ -47,7 +47,8 @@ def draw_tree_tokens(parents, draft_logits, temperature, uniforms,
     uint16); temperature: the float32 value used; uniforms: [N+1], u[c] draws
     node c's token. Status BAD_PARENT for an invalid tree, NONFINITE for a row
     with children that has NaN/+inf or no finite entry, DEGENERATE when a node
-    without replacement has more children than tokens of positive probability."""
+    without replacement has more children than tokens of positive probability;
+    the largest of these codes when several rows fail (rows are independent)."""
     n1 = len(parents)
     err = lambda st: DrawResult(st, np.full(n1, -1, np.int64))
     if not _valid_parents(parents):
@@ -56,23 +57,28 @@ def draw_tree_tokens(parents, draft_logits, temperature, uniforms,
     T = float(np.float32(temperature))
     tokens = np.full(n1, -1, np.int64)
     margin = float("inf")
+    status = O.TREE_OK            # rows are independent: the largest code of any row
     for j in range(n1):
         kids = [c for c in range(j + 1, n1) if int(parents[c]) == j]
         if not kids:
             continue
         q = O.tempered_softmax(zs[j], T)
         if q is None:
-            return err(O.TREE_NONFINITE)
+            status = max(status, O.TREE_NONFINITE)
+            continue
         for c in kids:
             y, m = O.inverse_cdf(q, float(uniforms[c]))
             if y < 0:
-                return err(O.TREE_DEGENERATE)
+                status = max(status, O.TREE_DEGENERATE)
+                break
             tokens[c] = y
             margin = min(margin, m)
             if mode == O.WITHOUT_REPLACEMENT:
                 if not q.sum() - q[y] > 0.0:     # no mass left for another sibling
                     if c != kids[-1]:
-                        return err(O.TREE_DEGENERATE)
+                        status = max(status, O.TREE_DEGENERATE)
                     break
                 q = O.draft_update_e2(q, y)
+    if status != O.TREE_OK:
+        return err(status)
     return DrawResult(O.TREE_OK, tokens, margin)

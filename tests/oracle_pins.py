@@ -417,6 +417,12 @@ def pin_draft_sampler_statuses():
     assert r.status == O.TREE_DEGENERATE
     r = DS.draw_tree_tokens(np.array([-1, 0, 0, 0]), zs, 1.0, u, O.WITH_REPLACEMENT)
     assert r.status == O.TREE_OK and list(r.tokens) == [-1, 1, 1, 1]
+    # a NaN row and a row with too many siblings: the larger code (DEGENERATE)
+    mixed = zs.copy()
+    mixed[0, 0] = np.nan
+    r = DS.draw_tree_tokens(np.array([-1, 0, 1, 1, 1]), np.vstack([mixed, zs[:1]]), 1.0,
+                            np.full(5, 0.5), O.WITHOUT_REPLACEMENT)
+    assert r.status == O.TREE_DEGENERATE and np.all(r.tokens == -1)
     # two children at V = 2 without replacement take both tokens
     r = DS.draw_tree_tokens(np.array([-1, 0, 0, 1]), zs, 1.0, u, O.WITHOUT_REPLACEMENT)
     assert r.status == O.TREE_OK and sorted(r.tokens[1:3]) == [0, 1]

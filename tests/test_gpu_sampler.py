@@ -130,6 +130,14 @@ def test_error_trees():
     tok, st = tv.draft_tokens(*args, W.WITH_REPLACEMENT)
     assert st.cpu().tolist() == [0, tv.TV_TREE_BAD_PARENT, tv.TV_TREE_NONFINITE, 0]
     check_sampler(*args, W.WITH_REPLACEMENT, label="errors with")
+    # a NaN row (the root's) and a row with three children over two tokens
+    par2 = torch.as_tensor(np.array([[-1, 0, 1, 1, 1]], np.int32), device=DEV)
+    zs2 = torch.as_tensor(rng.normal(0, 1.0, (1, 5, V)).astype(np.float32), device=DEV)
+    zs2[0, 0, 0] = float("nan")
+    u2 = torch.as_tensor(W.uniforms_np(rng, (1, 5)), device=DEV)
+    tok, st = tv.draft_tokens(par2, zs2, 1.0, u2, W.WITHOUT_REPLACEMENT)
+    assert st.cpu().tolist() == [tv.TV_TREE_DEGENERATE]
+    check_sampler(par2, zs2, 1.0, u2, W.WITHOUT_REPLACEMENT, label="mixed errors")
 
 
 @pytest.mark.parametrize("mode", MODES)
