@@ -263,6 +263,9 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=0)
     ap.add_argument("--mode", choices=["without", "with"], default="without")
     ap.add_argument("--tokenlevel-steps", type=int, default=20)
+    ap.add_argument("--parity-steps", type=int, default=0,
+                    help="also check every tree of this many more steps against the oracle "
+                         "(timed path: no theta, early rejection)")
     ap.add_argument("--deep-steps", type=int, default=8,
                     help="timed launches on Sequoia-scale trees (8 trees x 768 nodes, V=128256)")
     ap.add_argument("--sampler-steps", type=int, default=20,
@@ -411,6 +414,39 @@ def main():
 
     if args.sampler_steps > 0 and last is not None:
         res["draft_sampler"] = sampler_leg(last[0], args.sampler_steps, stream, elem)
+
+    if args.parity_steps > 0:
+        import multiprocessing as mp
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import parity  # noqa: E402  (test infrastructure: oracle comparison)
+        workers = args.cpu_workers or min(16, os.cpu_count() or 1)
+        tot = parity.ParityReport()
+        for k in range(args.parity_steps):
+            batch = W.make_batch(CFG, step=20_000 + k, device=dev, mode=mode, seed=1)
+            out = tv.verify_batch(batch["parents"], batch["tokens"], batch["target"],
+                                  batch["draft"], batch["temperature"], batch["uniforms"], mode,
+                                  want_nodes=True, want_theta=False, want_counters=True)
+            g = parity.host_outputs(out)
+            trees = [W.tree_numpy(batch, b) for b in range(B)]
+            with mp.get_context("fork").Pool(workers) as pool:
+                refs = pool.map(_oracle_one, [(t, batch["temperature"], mode) for t in trees])
+            for b, ref in enumerate(refs):
+                kind, msg, _ = parity.compare_tree(g, b, ref, False, False, "bf16")
+                tot.trees += 1
+                if kind == "exact":
+                    tot.exact += 1
+                elif kind == "near_tie":
+                    tot.near_ties += 1
+                else:
+                    tot.failures.append(f"step {k} tree {b}: {msg}")
+            print(f"parity step {k + 1}/{args.parity_steps}: {tot.summary()}", file=sys.stderr,
+                  flush=True)
+            del batch, out
+        res["parity_steps"] = {"steps": args.parity_steps, "trees": tot.trees,
+                               "exact": tot.exact, "near_ties": tot.near_ties,
+                               "failures": len(tot.failures)}
+        if tot.failures:
+            print("\n".join(tot.failures[:5]), file=sys.stderr)
 
     if args.cpu_sample > 0 and last is not None:
         workers = args.cpu_workers or min(16, os.cpu_count() or 1)
