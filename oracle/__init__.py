@@ -18,8 +18,15 @@ Contents:
   (Def. de_tree, Sec. 3.3), by inverse CDF at given uniforms.
 
 Pins (what the oracle is checked against, independent of itself) live in
-``tests/test_oracle_*.py`` and ``tests/golden/``. Every function here is pinned;
-none is "parity unpinned".
+``tests/oracle_pins.py`` (run by ``tests/test_oracle_pins.py``) and
+``tests/golden/``; ``tests/test_oracle_mutations.py`` plants plausible mistakes
+and checks that a pin catches each. Pinned: the verifiers' decisions,
+thresholds, chain rates and Y on the printed examples and exact laws; the work
+counters (rows consulted, residual updates, accepted leaf, tests) on
+hand-derived cases; the bfloat16 widening on all 65536 bit patterns; the
+per-tree error statuses of both verifiers and of the draft sampler; the
+committed sequence. The floating-point rounding of the kernels' sums has no
+pin of its own (only the tolerances and the near-tie rule apply).
 """
 
 from .tv_oracle import (  # noqa: F401
@@ -28,5 +35,5 @@ from .tv_oracle import (  # noqa: F401
     TREE_NONFINITE, TREE_DEGENERATE,
     NODE_UNTESTED, NODE_ACCEPTED, NODE_REJECTED, NODE_PRUNED,
     TreeResult, to_f64, tempered_softmax, inverse_cdf,
-    verify_tree, verify_tree_tokenlevel, algorithmic_bytes,
+    verify_tree, verify_tree_tokenlevel,
 )

@@ -480,17 +480,3 @@ def committed_sequence(parents, tokens, accepted_node: int, bonus_token: int):
         x = int(parents[x])
     chain.reverse()
     return chain, [int(tokens[c]) for c in chain] + [int(bonus_token)]
-
-
-# ---------------------------------------------------------------------------
-# Algorithmic bytes (what any implementation of the method must move)
-# ---------------------------------------------------------------------------
-
-def algorithmic_bytes(res: TreeResult, vocab: int, elem_bytes: int) -> dict:
-    """Bytes the method must read for one verified tree: both rows of every
-    consulted node (compulsory), the accepted leaf's target row (compulsory),
-    and both rows again for every residual update (re-scan)."""
-    row = vocab * elem_bytes
-    compulsory = 2 * row * res.rows_consulted + row * res.leaf_accepted
-    rescan = 2 * row * res.residual_passes
-    return {"compulsory": compulsory, "rescan": rescan, "total": compulsory + rescan}

@@ -450,11 +450,141 @@ def pin_committed_sequence():
         assert not nodes or int(p[nodes[0]]) == 0
 
 
+# ---------------------------------------------------------------------------
+# Bookkeeping the kernels report: work counters, input widening, statuses
+# ---------------------------------------------------------------------------
+
+def pin_counters_worked_example():
+    """Work counters on the Sec. 3.2 tree, derived by hand from their
+    definitions: rows consulted = internal nodes that are proper ancestors of
+    a tested node; residual updates = rejections followed by Eq. (e1)-(e3);
+    leaf accepted = the accepted node has no children; tests = nodes compared
+    with their uniform.
+
+    * Every drafted node rejected (uniforms just below 1): tests X3, X4, X1,
+      X5, X2 (X2's rate is 1, so it is accepted); their proper ancestors are
+      X0, X1, X2; updates after X3, X4 (at X1), X1 (at X0) and X5 (at X2):
+      (3, 4, 0, 5).
+    * All uniforms 0: X3 (rate 2/3) is accepted at once; ancestors X0, X1; a
+      leaf: (2, 0, 1, 1).
+    * Token-level, every candidate rejected: X1 (1/2) rejected, update at X0;
+      X2 (rate 1 on the residual) accepted; X5 (1/2) rejected, update at X2; Y
+      from X2's residual. Tested X1, X2, X5 with ancestors X0, X2: (2, 2, 0, 3).
+    * Token-level, all uniforms 0: X1 then X3 (rate 1) accepted; a leaf:
+      (2, 0, 1, 2)."""
+    par, tok, zb, zs, T = W.worked_example()
+    hi = np.full(6, ALMOST_ONE, np.float32)
+    hi[0] = 0.5
+    lo = np.zeros(6, np.float32)
+    cases = [(O.verify_tree, hi, (3, 4, 0, 5)), (O.verify_tree, lo, (2, 0, 1, 1)),
+             (O.verify_tree_tokenlevel, hi, (2, 2, 0, 3)),
+             (O.verify_tree_tokenlevel, lo, (2, 0, 1, 2))]
+    for ver, u, want in cases:
+        r = ver(par, tok, zb, zs, T, u, O.WITHOUT_REPLACEMENT)
+        assert r.status == O.TREE_OK
+        assert tuple(r.counters) == want, (ver.__name__, tuple(r.counters), want)
+
+
+def pin_counters_identical_models():
+    """M_s = M_b on a complete binary tree of depth 3: the first leaf (node 7)
+    is accepted with rate 1 after no update; its proper ancestors 0, 1, 3 are
+    the rows consulted: counters (3, 0, 1, 1). The token-level verifier
+    accepts 1, 3, 7 in turn: (3, 0, 1, 3)."""
+    rng = np.random.default_rng(11)
+    par = W.binary_parents(3)
+    n1, V = len(par), 17
+    z = rng.normal(0, 2, (n1, V))
+    tok = rng.integers(0, V, n1).astype(np.int32)
+    u = W.uniforms_np(rng, n1)
+    r = O.verify_tree(par, tok, z, z.copy(), 1.0, u, O.WITH_REPLACEMENT)
+    assert tuple(r.counters) == (3, 0, 1, 1), tuple(r.counters)
+    r = O.verify_tree_tokenlevel(par, tok, z, z.copy(), 1.0, u, O.WITH_REPLACEMENT)
+    assert r.accepted_node == 7 and tuple(r.counters) == (3, 0, 1, 3), tuple(r.counters)
+
+
+def pin_bf16_widening():
+    """bfloat16 logits arrive as 16-bit patterns: the top half of an IEEE
+    float32. All 65536 patterns widen to what torch's own bfloat16 -> float32
+    conversion gives (NaN patterns to NaN), and a few values follow from the
+    format by hand: 0x3FC0 = 1.5, 0xC000 = -2, 0x7F80 = +inf, 0xFF80 = -inf,
+    0x0001 = 2^-133 (the smallest subnormal), 0x0080 = 2^-126."""
+    import torch
+    bits = np.arange(65536, dtype=np.uint16)
+    got = O.to_f64(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).float().double().numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    hand = {0x3FC0: 1.5, 0xC000: -2.0, 0x7F80: np.inf, 0xFF80: -np.inf,
+            0x0001: 2.0 ** -133, 0x0080: 2.0 ** -126, 0x0000: 0.0}
+    for b, v in hand.items():
+        assert O.to_f64(np.array([b], np.uint16))[0] == v, (hex(b), v)
+    # float32 rows are widened as they are
+    f = np.array([0.1, -3.5, 1e-40], np.float32)
+    assert np.array_equal(O.to_f64(f), f.astype(np.float64))
+
+
+def pin_verifier_statuses():
+    """Per-tree statuses of both verifiers on hand-made cases: a root whose
+    parent is not -1 or a link that does not point to an earlier node
+    (BAD_PARENT, before token checks), a drafted token outside [0, V)
+    (BAD_TOKEN), two siblings with one token without replacement (DUP_SIBLING;
+    fine with replacement), a NaN, +inf or all--inf row with children and a
+    drafted token whose draft logit is -inf (NONFINITE). Rows the verifier
+    never reads (a leaf's draft row, a rejected leaf's target row) may hold
+    anything."""
+    par, tok, zb, zs, T = W.worked_example()
+    u = np.full(6, ALMOST_ONE, np.float32)
+    u[0] = 0.5
+    W_ = O.WITHOUT_REPLACEMENT
+    for ver in (O.verify_tree, O.verify_tree_tokenlevel):
+        def st(p=par, t=tok, b=zb, s=zs, mode=W_):
+            return ver(np.asarray(p), np.asarray(t), b, s, T, u, mode).status
+        base = ver(par, tok, zb, zs, T, u, W_)
+        assert base.status == O.TREE_OK
+        assert st(p=[0, 0, 0, 1, 1, 2]) == O.TREE_BAD_PARENT
+        assert st(p=[-1, 0, 0, 3, 1, 2]) == O.TREE_BAD_PARENT
+        assert st(p=[-1, 0, 0, 1, 1, -1]) == O.TREE_BAD_PARENT
+        assert st(p=[-1, 0, 0, 3, 1, 2], t=[0, 0, 2, 1, 2, 7]) == O.TREE_BAD_PARENT
+        assert st(t=[0, 0, 2, 1, 2, 3]) == O.TREE_BAD_TOKEN
+        assert st(t=[0, -1, 2, 1, 2, 0]) == O.TREE_BAD_TOKEN
+        assert st(t=[5, 0, 2, 1, 2, 0]) == O.TREE_OK          # the root's token is unused
+        assert st(t=[0, 0, 2, 1, 1, 0]) == O.TREE_DUP_SIBLING  # X3 and X4 both b
+        assert st(t=[0, 0, 2, 1, 1, 0], mode=O.WITH_REPLACEMENT) == O.TREE_OK
+        for bad in (np.nan, np.inf):
+            for rows, which in ((zb, "target"), (zs, "draft")):
+                z = rows.copy()
+                z[0, 1] = bad
+                kw = {"b": z} if which == "target" else {"s": z}
+                assert st(**kw) == O.TREE_NONFINITE, (ver.__name__, bad, which)
+        z = zb.copy()
+        z[0, :] = -np.inf
+        assert st(b=z) == O.TREE_NONFINITE
+        z = zs.copy()
+        z[0, 0] = -np.inf           # X1's token a cannot be drafted
+        assert st(s=z) == O.TREE_NONFINITE
+        # a leaf's draft row is never read
+        z = zs.copy()
+        z[3, :] = np.nan
+        r = ver(par, tok, zb, z, T, u, W_)
+        assert r.status == O.TREE_OK and r.accepted_node == base.accepted_node
+    # Traversal Verification rejects X3 (a leaf) here: its target row is not read
+    z = zb.copy()
+    z[3, :] = np.nan
+    r = O.verify_tree(par, tok, z, zs, T, u, W_)
+    assert r.status == O.TREE_OK and r.accepted_node == 2
+    # ... but it is read when X3 is accepted (Y ~ its target)
+    r = O.verify_tree(par, tok, z, zs, T, np.zeros(6, np.float32), W_)
+    assert r.status == O.TREE_NONFINITE
+
+
 FAST_PINS = [pin_worked_example_trace, pin_worked_example_tokenlevel, pin_worked_example_law,
              pin_single_token_table1, pin_rrsw_example, pin_tempered_softmax_inverse,
              pin_inverse_cdf_law, pin_identical_models, pin_depth1_equals_rrsw,
              pin_invariants, pin_early_rejection_worked_example, pin_early_rejection_sound,
-             pin_draft_sampler_law, pin_draft_sampler_statuses, pin_committed_sequence]
+             pin_draft_sampler_law, pin_draft_sampler_statuses, pin_committed_sequence,
+             pin_counters_worked_example, pin_counters_identical_models, pin_bf16_widening,
+             pin_verifier_statuses]
 ENUM_PINS = [pin_lossless_exact, pin_lossless_irregular_T07, pin_chain_optimality]
 ALL_PINS = FAST_PINS + ENUM_PINS
 

@@ -96,6 +96,64 @@ def _early_any_child(res, children, alive, p, uniforms, j):
         res.early_nodes.append(j)
 
 
+def _finish_parents_only(res, children, depth, parents, uniforms):
+    """Counts only the parents of tested nodes as consulted rows."""
+    res = _finish_orig(res, children, depth, parents, uniforms)
+    res.rows_consulted = len({int(parents[t]) for t in res.test_order})
+    return res
+
+
+def _finish_counts_accepted_row(res, children, depth, parents, uniforms):
+    """Counts the accepted node's own row as consulted."""
+    res = _finish_orig(res, children, depth, parents, uniforms)
+    seen = set()
+    for t in res.test_order:
+        a = int(parents[t])
+        while a >= 0:
+            seen.add(a)
+            a = int(parents[a])
+    seen.add(res.accepted_node)
+    res.rows_consulted = len(seen)
+    return res
+
+
+def _finish_tests_off_by_one(res, children, depth, parents, uniforms):
+    res = _finish_orig(res, children, depth, parents, uniforms)
+    res.tests = max(0, res.tests - 1)
+    return res
+
+
+def _finish_leaf_flag_inverted(res, children, depth, parents, uniforms):
+    res = _finish_orig(res, children, depth, parents, uniforms)
+    res.leaf_accepted = 1 - res.leaf_accepted
+    return res
+
+
+_finish_orig = O._finish
+
+
+def _to_f64_as_fp16(logits):
+    a = np.asarray(logits)
+    if a.dtype == np.uint16:
+        return a.view(np.float16).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def _to_f64_low_half(logits):
+    a = np.asarray(logits)
+    if a.dtype == np.uint16:
+        return a.astype(np.uint32).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def _structure_no_dup_check(parents, tokens, V, mode):
+    return _structure_orig(parents, tokens, V, O.WITH_REPLACEMENT)
+
+
+def _structure_token_bound_inclusive(parents, tokens, V, mode):
+    return _structure_orig(parents, tokens, V + 1, mode)
+
+
 MUTATIONS = {
     "e1 drops the p factor": ("residual_e1", _e1_without_p),
     "e1 target and draft swapped": ("residual_e1", _e1_swapped),
@@ -111,6 +169,14 @@ MUTATIONS = {
     "RRS residual not normalised": ("rrs_residual", _residual_without_norm),
     "early rejection with u below p": ("_early_rejection", _early_when_below),
     "early rejection with children left": ("_early_rejection", _early_any_child),
+    "consulted rows: parents of tested nodes only": ("_finish", _finish_parents_only),
+    "consulted rows include the accepted node": ("_finish", _finish_counts_accepted_row),
+    "tests counter one short": ("_finish", _finish_tests_off_by_one),
+    "leaf-accepted flag inverted": ("_finish", _finish_leaf_flag_inverted),
+    "bf16 read as fp16": ("to_f64", _to_f64_as_fp16),
+    "bf16 widened into the low half": ("to_f64", _to_f64_low_half),
+    "duplicate siblings not detected": ("_structure", _structure_no_dup_check),
+    "token bound V accepted": ("_structure", _structure_token_bound_inclusive),
 }
 
 
