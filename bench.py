@@ -30,32 +30,66 @@ HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
 SLEEP_CYCLES = 2_000_000     # about 1 ms of GPU clock ahead of each timed launch
 CFG = 5
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "tv_verify_256trees_n64_v128256_hbm_counters.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2505_12398_amd", "csrc", "tv_kernels.hip")
+PROFILE_TRACE = os.path.join(ROOT, "profiles", "tv_verify_256trees_n64_v128256_kernel_trace.md")
+CSRC = os.path.join(ROOT, "paper_2505_12398_amd", "csrc")
+HEADER = os.path.join(ROOT, "include", "tv.h")
 METRIC = ("verified trees/sec + achieved HBM GB/s (% peak), 64-node trees, V=128256, bf16")
 
 
 def kernel_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of every source the library is built from (the kernels, their
+    launch code and the C-ABI) and of its header: a profile taken on other
+    sources no longer describes this build."""
+    h = hashlib.sha256()
+    for path in sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)) + [HEADER]:
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the kernel as it is now; else None."""
-    if not os.path.exists(PROFILE_COUNTERS):
+def _profile_value(path, key):
+    """A number from a committed rocprofv3 summary, if the summary was taken on
+    the sources as they are now; else None."""
+    if not os.path.exists(path):
         return None
-    text = open(PROFILE_COUNTERS).read()
+    text = open(path).read()
     m = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
-    t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    t = re.search(rf"{key}:\s*([0-9.eE+]+)", text)
     if not m or not t or m.group(1) != kernel_hash():
         return None
     return float(t.group(1))
 
 
-def algorithmic_bytes(counters, vocab, elem_bytes, num_nodes):
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary."""
+    return _profile_value(PROFILE_COUNTERS, "hbm_bytes_per_launch")
+
+
+def traced_kernel_us():
+    """Mean duration of the verify kernel alone (no initialisation kernel, no
+    launch gap) from the committed rocprofv3 kernel trace."""
+    return _profile_value(PROFILE_TRACE, "verify_kernel_mean_us")
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def algorithmic_bytes(counters, vocab, elem_bytes, num_nodes, status=None):
     """Bytes the method must move for one launch: both rows of every consulted
     node, the accepted leaf's target row, both rows again per residual update,
-    plus the per-node inputs and outputs."""
+    plus the per-node inputs and outputs. Counters of trees whose status is
+    not OK are excluded (an error tree reports zeros)."""
+    if status is not None:
+        counters = counters[status == 0]
     c = counters.sum(dim=0).tolist()
     row = vocab * elem_bytes
     B = counters.shape[0]
@@ -246,6 +280,72 @@ def sampler_leg(batch, steps: int, stream, elem: int) -> dict:
                               "failures": fail}}
 
 
+def config_leg(cfg_id: int, steps: int, tl_steps: int, mode: int, stream, batch=None,
+               label=None) -> dict:
+    """One workload at its full size (or ``batch`` trees of it): tv_verify on
+    the timed path (no theta: early rejection) over ``steps`` launches with
+    fresh seeds, the token-level verifier over ``tl_steps`` launches on the
+    same trees and uniforms, algorithmic bytes and acceptance lengths. A
+    512 MiB buffer is written before each timed launch so that the launch reads
+    its rows from HBM, not from the 256 MiB cache in front of it."""
+    import torch
+
+    import paper_2505_12398_amd as tv
+    import workloads as W
+    cfg = W.CONFIGS[cfg_id]
+    dev = torch.device("cuda", 0)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    B = batch or cfg.batch
+    n1, V = cfg.n_nodes + 1, cfg.vocab
+    elem = 2 if cfg.dtype == "bf16" else 4
+    ws, _ = tv.workspace_tensor(B, n1, V, dev)
+    res = {"tv": [], "tl": []}
+    for s in range(max(steps, tl_steps) + 1):          # launch 0 is an untimed warmup
+        bt = W.make_batch(cfg_id, step=30_000 + s, device=dev, mode=mode, batch=B, seed=2)
+        for tl in (False, True):
+            if s > (tl_steps if tl else steps):
+                continue
+            flush.fill_(s & 0xFF)
+            torch.cuda.synchronize()
+            ev0 = torch.cuda.Event(enable_timing=True)
+            ev1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(SLEEP_CYCLES)
+            ev0.record(stream)
+            out = tv.verify_batch(bt["parents"], bt["tokens"], bt["target"], bt["draft"],
+                                  bt["temperature"], bt["uniforms"], mode, tokenlevel=tl,
+                                  want_nodes=False, want_counters=True,
+                                  stream=stream.cuda_stream, workspace=ws)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            if s == 0:
+                continue
+            st = out.status
+            if int((st != tv.TV_TREE_OK).sum().item()):
+                raise RuntimeError(f"config {cfg_id}: trees with error status")
+            res["tl" if tl else "tv"].append(
+                (ev0.elapsed_time(ev1), algorithmic_bytes(out.counters, V, elem, n1, st)["total"],
+                 out.accept_len.float().mean().item() + 1.0))
+        del bt
+    del flush
+
+    def mean(xs):
+        return sum(xs) / max(1, len(xs))
+    ms = mean([r[0] for r in res["tv"]])
+    alg = mean([r[1] for r in res["tv"]])
+    acc_tv = mean([r[2] for r in res["tv"][:tl_steps]])
+    acc_tl = mean([r[2] for r in res["tl"]])
+    gbps = alg / (ms * 1e-3) / 1e9
+    return {"workload": label or cfg.name, "trees": B, "rows_per_tree": n1, "vocab": V,
+            "dtype": cfg.dtype, "temperature": cfg.temperature, "steps": steps,
+            "ms_per_step": ms, "trees_per_s": B / (ms * 1e-3),
+            "algorithmic_bytes_per_launch": alg, "achieved_GBps": gbps,
+            "frac": gbps / HBM_PEAK_GBPS,
+            "tokenlevel_ms_per_step": mean([r[0] for r in res["tl"]]),
+            "accept_len_mean": {"traversal": acc_tv, "tokenlevel": acc_tl,
+                                "delta_pct": 100.0 * (acc_tv / acc_tl - 1.0) if acc_tl else None},
+            "cache": "512 MiB written before each launch (cold rows)"}
+
+
 def _oracle_one(args):
     (par, tok, zb, zs, u), T, mode = args
     from oracle import verify_tree
@@ -270,6 +370,9 @@ def main():
                     help="timed launches on Sequoia-scale trees (8 trees x 768 nodes, V=128256)")
     ap.add_argument("--sampler-steps", type=int, default=20,
                     help="timed launches of the draft-tree token sampler on the same trees")
+    ap.add_argument("--config-steps", type=int, default=10,
+                    help="timed launches per smaller workload (chain, binary tree, irregular "
+                         "tree) and of the one-tree latency leg (0: skip them)")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="only run plain device-to-device copies of this size (to scale "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -334,7 +437,9 @@ def main():
     for s in range(args.steps):
         ms, batch, out = one_step(s)
         times.append(ms)
-        nb = algorithmic_bytes(out.counters, V, elem, n1)
+        if int((out.status == tv.TV_TREE_ABORTED).sum().item()):
+            raise RuntimeError("a timed launch gave up (TV_TREE_ABORTED)")
+        nb = algorithmic_bytes(out.counters, V, elem, n1, out.status)
         nbytes.append(nb)
         acc_tv.append(out.accept_len.float().mean().item() + 1.0)
         statuses.append(int((out.status != tv.TV_TREE_OK).sum().item()))
@@ -348,6 +453,7 @@ def main():
     alg_total = sum(b["total"] for b in nbytes) / len(nbytes)
     achieved = alg_total / (ms_mean * 1e-3) / 1e9
     traffic = measured_traffic()
+    kernel_us = traced_kernel_us()
 
     # token-level baseline on the same trees and uniforms (common random numbers)
     tl_times, acc_tl, acc_tv_same = [], [], []
@@ -391,6 +497,14 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_total,
             "kernel": "verify_kernel<uint16_t, FastArith, 128> (tv_verify)",
+            "timing": "HIP events around each tv_verify call (initialisation kernel, launch "
+                      "gap and verify kernel)",
+            "kernel_only": None if kernel_us is None else {
+                "verify_kernel_mean_us": kernel_us,
+                "achieved": alg_total / (kernel_us * 1e-6) / 1e9,
+                "frac": alg_total / (kernel_us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+                "source": "committed rocprofv3 kernel trace of these sources"},
+            "sources_sha256_16": kernel_hash(),
         },
         "nominal_input_GBps": 2 * B * n1 * V * elem / (ms_mean * 1e-3) / 1e9,
         "trees_with_error_status": sum(statuses),
@@ -411,6 +525,17 @@ def main():
 
     if args.deep_steps > 0:
         res["deep_trees"] = deep_leg(args.deep_steps, mode, stream, elem, V)
+
+    if args.config_steps > 0:
+        res["configs"] = {}
+        for cid in (2, 3, 4):
+            res["configs"][str(cid)] = config_leg(cid, args.config_steps,
+                                                  max(1, args.config_steps // 2), mode, stream)
+            print(f"config {cid} leg done", file=sys.stderr, flush=True)
+        res["single_tree_latency"] = config_leg(
+            CFG, 2 * args.config_steps, args.config_steps, mode, stream, batch=1,
+            label=cfg.name.replace("B256", "B1") + " (one tree per call: latency)")
+        print("single-tree leg done", file=sys.stderr, flush=True)
 
     if args.sampler_steps > 0 and last is not None:
         res["draft_sampler"] = sampler_leg(last[0], args.sampler_steps, stream, elem)
@@ -462,10 +587,19 @@ def main():
         torch.cuda.synchronize()
         tps, secs, reps = cpu_baseline(batch, {"timed": outs[False], "theta": outs[True]},
                                        sample, workers)
+        # one process, one core: the oracle on the first trees, in this process
+        n_single = min(8, B)
+        t0 = time.perf_counter()
+        for b in range(n_single):
+            _oracle_one((W.tree_numpy(batch, b), batch["temperature"], mode))
+        per_core = n_single / (time.perf_counter() - t0)
         res["cpu_baseline"] = {
             "value": tps, "unit": "trees/s", "cores": workers, "kind": "oracle",
             "sample": f"first {sample} trees of timed step {args.steps - 1} "
                       f"({secs:.1f} s wall, float64 numpy, one process per core)",
+            "per_core": {"value": per_core, "unit": "trees/s",
+                         "sample": f"first {n_single} trees of the same step, one process"},
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
         }
         rep, rth = reps["timed"], reps["theta"]
         res["parity_sample"] = {"trees": rep.trees, "exact": rep.exact,

@@ -11,6 +11,15 @@
 namespace tv {
 
 int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
+  const int st = validate_args(a);
+  if (st != TV_OK || a.batch == 0) return st;
+  if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 256 ||
+      workspace_bytes < workspace_layout(a.batch, a.vocab).bytes)
+    return TV_ERR_WORKSPACE;
+  return TV_OK;
+}
+
+int validate_args(const VerifyArgs& a) {
   if (a.batch < 0 || a.num_nodes < 1 || a.vocab < 2) return TV_ERR_INVALID_ARG;
   if (a.dtype != TV_DTYPE_BF16 && a.dtype != TV_DTYPE_F32) return TV_ERR_INVALID_ARG;
   if (a.mode != TV_SIBLINGS_WITHOUT_REPLACEMENT && a.mode != TV_SIBLINGS_WITH_REPLACEMENT)
@@ -34,9 +43,6 @@ int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes) {
                             a.bonus_token, a.status, a.node_theta, a.p_init, a.counters};
   for (const void* p : int_ptrs)
     if (reinterpret_cast<uintptr_t>(p) % 4) return TV_ERR_INVALID_ARG;
-  if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 256 ||
-      workspace_bytes < workspace_layout(a.batch, a.vocab).bytes)
-    return TV_ERR_WORKSPACE;
   return TV_OK;
 }
 

@@ -65,6 +65,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include <mutex>
 #include <type_traits>
@@ -1300,16 +1301,18 @@ __device__ __forceinline__ bool await_part(const PP& P, const SegPart* part, int
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     if (lane < G) ok = tags_are(w, tag);
     if (__ballot(!ok) == 0) return true;
-    __builtin_amdgcn_s_sleep(1);
-    if ((it & 15) == 15) {
+    // the abort flag and the clock are checked every 16th failed poll (every
+    // failed poll with a wait limit of 0)
+    if ((it & 15) == 15 || P.spin_limit == 0) {
       uint32_t ab = 0;
       if (lane == 0) ab = ld_rlx(ws_abort(P));
       if (__shfl(ab, 0, 64)) return false;
-      if (wall_clock64() - t0 > P.spin_limit) {
+      if (wall_clock64() - t0 >= P.spin_limit) {
         if (lane == 0) st_rlx(ws_abort(P), 1u);
         return false;
       }
     }
+    __builtin_amdgcn_s_sleep(1);
   }
 }
 
@@ -1842,11 +1845,10 @@ __device__ __forceinline__ void await_desc(Lds<WgScratch>& ws, const Params& P, 
       }
       return;
     }
-    __builtin_amdgcn_s_sleep(2);
-    if ((it & 15) == 15) {
+    if ((it & 15) == 15 || P.spin_limit == 0) {
       uint32_t ab = 0;
       if (lane == 0) ab = ld_rlx(ws_abort(P));
-      if (__shfl(ab, 0, 64) || wall_clock64() - t0 > P.spin_limit) {
+      if (__shfl(ab, 0, 64) || wall_clock64() - t0 >= P.spin_limit) {
         if (lane == 0) {
           st_rlx(ws_abort(P), 1u);
           ws.help_state = 2;
@@ -1854,6 +1856,7 @@ __device__ __forceinline__ void await_desc(Lds<WgScratch>& ws, const Params& P, 
         return;
       }
     }
+    __builtin_amdgcn_s_sleep(2);
   }
 }
 
@@ -2013,22 +2016,36 @@ __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
 // Kernels
 // ---------------------------------------------------------------------------
 
-// Clears the abort flag and the partials (tag 0: no batch yet) and marks every
-// tree aborted until it is finished.
+// Clears the abort flag and the partials (tag 0: no batch yet) and gives
+// every tree the outputs of an aborted tree (status TV_TREE_ABORTED, -1
+// sentinels, counters 0), which finish_tree overwrites for the trees it
+// finishes. Every loop is grid-stride, so any grid covers any batch.
 __global__ void __launch_bounds__(256) init_kernel(Params P) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
   if (i == 0) *ws_abort(P) = 0u;
   uint64_t* parts = reinterpret_cast<uint64_t*>(P.ws + P.off_parts);
-  for (size_t k = i; k < P.parts_words; k += static_cast<size_t>(gridDim.x) * blockDim.x)
-    parts[k] = 0u;
+  for (size_t k = i; k < P.parts_words; k += stride) parts[k] = 0u;
   uint64_t* desc = reinterpret_cast<uint64_t*>(P.ws + P.off_desc);
-  for (size_t k = i; k < P.desc_words; k += static_cast<size_t>(gridDim.x) * blockDim.x)
-    desc[k] = 0u;
-  if (i < P.batch) {
-    P.status[i] = TV_TREE_ABORTED;
-    P.accept_len[i] = -1;
-    P.accepted_node[i] = -1;
-    P.bonus_token[i] = -1;
+  for (size_t k = i; k < P.desc_words; k += stride) desc[k] = 0u;
+  const size_t nb = static_cast<size_t>(P.batch);
+  for (size_t b = i; b < nb; b += stride) {
+    P.status[b] = TV_TREE_ABORTED;
+    P.accept_len[b] = -1;
+    P.accepted_node[b] = -1;
+    P.bonus_token[b] = -1;
+    if (P.counters) {
+#pragma unroll
+      for (int c = 0; c < TV_NUM_COUNTERS; ++c) P.counters[b * TV_NUM_COUNTERS + c] = 0;
+    }
+  }
+  if (P.node_state || P.node_theta || P.p_init) {
+    const size_t nn = nb * static_cast<size_t>(P.num_nodes);
+    for (size_t k = i; k < nn; k += stride) {
+      if (P.node_state) P.node_state[k] = TV_NODE_UNTESTED;
+      if (P.node_theta) P.node_theta[k] = -1.0f;
+      if (P.p_init) P.p_init[k] = -1.0f;
+    }
   }
 }
 
@@ -2084,6 +2101,20 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
 // with few elements the per-element rounding of the fast path does not average.
 constexpr int kPreciseBelowVocab = 16384;
 
+// Milliseconds a wait inside the verifier may last before the launch is
+// abandoned: 4000, or the value of the environment variable TV_WAIT_LIMIT_MS
+// (a decimal integer in [0, 60000]; 0 abandons a launch at the first wait
+// that is not satisfied at once, which tests of the abandon path use).
+long long wait_limit_ms() {
+  long long ms = 4000;
+  if (const char* e = getenv("TV_WAIT_LIMIT_MS")) {
+    char* end = nullptr;
+    const long v = strtol(e, &end, 10);
+    if (end != e && *end == '\0' && v >= 0 && v <= 60000) ms = v;
+  }
+  return ms;
+}
+
 template <typename T, class A, int kCap>
 int launch_typed(Params P, A ar, hipStream_t stream) {
   // device properties and the kernel's occupancy, queried once per device
@@ -2138,11 +2169,11 @@ int launch_typed(Params P, A ar, hipStream_t stream) {
   if (gx > gmax) gx = gmax;
   if (gx < G) gx = G;
   P.Gx = static_cast<int>(gx);
-  P.spin_limit = static_cast<long long>(clock_khz) * 1000LL * 4;   // 4 s
+  P.spin_limit = static_cast<long long>(clock_khz) * wait_limit_ms();
   long long init_n = static_cast<long long>(P.parts_words);
   if (init_n < P.batch) init_n = P.batch;
   long long init_blocks = (init_n + 255) / 256;
-  if (init_blocks > 1024) init_blocks = 1024;     // the partials are cleared in a grid-stride loop
+  if (init_blocks > 1024) init_blocks = 1024;     // every loop of init_kernel is grid-stride
   hipLaunchKernelGGL(init_kernel, dim3(static_cast<unsigned>(init_blocks)), dim3(256), 0, stream,
                      P);
   if (hipGetLastError() != hipSuccess) return TV_ERR_HIP;
@@ -2350,9 +2381,11 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   // One read of the row: wave w sums chunks w, w + 4, ..., with
   // kRowChunksInFlight chunks' loads issued together; the chunks of one such
   // round share the frame of their maximum. Chunk sums are fp32 on the fast
-  // path (a chunk is under 1% of a row's weight at the vocabularies it
-  // serves, so its rounding moves a chunk boundary by far less than the
-  // near-tie band) and fp64 on the precise one.
+  // path and fp64 on the precise one. The fp32 butterfly over a chunk's 64
+  // unit sums has a relative error of at most about 6 * 2^-24 of the chunk's
+  // sum, hence of the row's total W whatever share of the row the chunk
+  // holds; that is below the 1e-6 * W near-tie band, so it can move a draw
+  // only at a near-tie.
   float wmax = -INFINITY;
   for (int c0 = wave; c0 < C; c0 += kNW * kRowChunksInFlight) {
     float x[kRowChunksInFlight][RowWeights<T, A>::E];

@@ -70,7 +70,9 @@ inline WorkspaceLayout workspace_layout(int32_t batch, int32_t vocab) {
   return L;
 }
 
-// Argument checks that need no GPU. Returns a tv_status_t.
+// Argument checks that need no GPU, without / with the caller's workspace.
+// Return a tv_status_t.
+int validate_args(const VerifyArgs& a);
 int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes);
 
 struct SampleArgs {

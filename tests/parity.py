@@ -146,16 +146,65 @@ def run_gpu(batch: dict, tokenlevel: bool, p_init: bool = False, theta: bool = T
     return host_outputs(out)
 
 
+_POOL_DATA = None
+
+
+def _pool_oracle(args):
+    b, tokenlevel = args
+    par, tok, zb, zs, u, T, mode = _POOL_DATA
+    fn = verify_tree_tokenlevel if tokenlevel else verify_tree
+    r = fn(par[b], tok[b], zb[b], zs[b], T, u[b], mode)
+    r.y_weights = None           # not compared; keeps the result small to send back
+    return r
+
+
+def host_batch(batch: dict):
+    """Host copies of a whole batch for the oracle (bf16 logits as uint16 bits)."""
+    import torch
+
+    def rows(t):
+        t = t.detach().cpu()
+        if t.dtype == torch.bfloat16:
+            return t.view(torch.int16).numpy().view(np.uint16)
+        return t.numpy()
+
+    return (batch["parents"].cpu().numpy(), batch["tokens"].cpu().numpy(),
+            rows(batch["target"]), rows(batch["draft"]), batch["uniforms"].cpu().numpy(),
+            batch["temperature"], batch["mode"])
+
+
+def oracle_many(batch: dict, trees, tokenlevels=(False, True), workers: int = 16,
+                host=None) -> dict:
+    """Oracle results of the listed trees for each verifier, computed by a pool
+    of forked worker processes that only run the numpy oracle (the inputs are
+    copied to host memory first and inherited, never sent). Returns
+    {tokenlevel: [results in the order of trees]}."""
+    import multiprocessing as mp
+    global _POOL_DATA
+    _POOL_DATA = host if host is not None else host_batch(batch)
+    trees = list(trees)
+    jobs = [(b, tl) for tl in tokenlevels for b in trees]
+    try:
+        with mp.get_context("fork").Pool(workers) as pool:
+            res = pool.map(_pool_oracle, jobs, chunksize=1)
+    finally:
+        _POOL_DATA = None
+    n = len(trees)
+    return {tl: res[k * n:(k + 1) * n] for k, tl in enumerate(tokenlevels)}
+
+
 def check(batch: dict, tokenlevel: bool, trees=None, p_init: bool = False,
-          gpu: dict | None = None, label: str = "", theta: bool = True) -> ParityReport:
+          gpu: dict | None = None, label: str = "", theta: bool = True,
+          refs=None) -> ParityReport:
     """Run the HIP verifier on the whole batch (unless ``gpu`` outputs are
-    given) and compare the listed trees (all by default) with the oracle."""
+    given) and compare the listed trees (all by default) with the oracle
+    (computed here, or given in ``refs`` in the order of ``trees``)."""
     if gpu is None:
         gpu = run_gpu(batch, tokenlevel, p_init, theta)
     B = batch["parents"].shape[0]
     rep = ParityReport()
-    for b in (range(B) if trees is None else trees):
-        ref = oracle_tree(batch, b, tokenlevel)
+    for k, b in enumerate(range(B) if trees is None else trees):
+        ref = oracle_tree(batch, b, tokenlevel) if refs is None else refs[k]
         kind, msg, worst = compare_tree(gpu, b, ref, tokenlevel, p_init,
                                         batch.get("dtype", "f32"))
         rep.trees += 1
