@@ -187,6 +187,28 @@ int tv_verify(int32_t batch, int32_t num_nodes, int32_t vocab,
               hipStream_t stream);
 
 /*
+ * tv_verify without a caller workspace, for callers that cannot allocate
+ * device memory or cannot pass a workspace: code that is being captured into
+ * a HIP graph, serving loops and harnesses that forbid allocation. Same
+ * arguments, outputs and per-tree statuses as tv_verify, minus workspace and
+ * workspace_bytes. The call allocates nothing: it uses a device scratch array
+ * of 3 MiB that the library holds on every device it runs on until the
+ * process ends (its address is looked up once per device, on the first call
+ * there). That covers every size the limits below allow; a size needing more
+ * would return TV_ERR_UNSUPPORTED. Every call on one device shares that
+ * device's scratch, and each call clears what it needs: calls on one device
+ * must not overlap (calls on different streams of one device race; order them,
+ * e.g. on one stream). Calls on different devices are independent.
+ */
+int tv_verify_noalloc(int32_t batch, int32_t num_nodes, int32_t vocab,
+                      const int32_t* parents, const int32_t* tokens,
+                      const void* target_logits, const void* draft_logits, int32_t dtype,
+                      float temperature, const float* uniforms, int32_t mode,
+                      int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
+                      int32_t* status, int8_t* node_state, float* node_theta, float* p_init,
+                      int32_t* counters, hipStream_t stream);
+
+/*
  * Token-level tree verification (Sec. 2.2): starting at the root, the children
  * of the current node are tested in index order with recursive rejection
  * sampling (Algorithm 2; without replacement per `mode`); an accepted child

@@ -16,7 +16,7 @@ from ._lib import (  # noqa: F401
     TV_NODE_UNTESTED, TV_NODE_ACCEPTED, TV_NODE_REJECTED, TV_NODE_PRUNED,
     TV_MAX_BATCH, TV_MAX_NODES, TV_MAX_VOCAB, TV_MAX_VOCAB_F32, TV_NUM_COUNTERS,
     LIB_PATH, TvError, load_library,
-    tv_workspace_size, tv_verify, tv_verify_tokenlevel, tv_status_string, tv_draft_tokens,
+    tv_workspace_size, tv_verify, tv_verify_noalloc, tv_verify_tokenlevel, tv_status_string, tv_draft_tokens,
     draft_tokens, tv_commit_paths, commit_paths, TV_COMMIT_OVERFLOW, TV_COMMIT_INCONSISTENT,
     VerifyOutputs, verify_batch, workspace_tensor,
 )

@@ -62,6 +62,8 @@ def load_library(path: str = LIB_PATH):
             fn = getattr(lib, name)
             fn.argtypes = _VERIFY_ARGTYPES
             fn.restype = ctypes.c_int
+        lib.tv_verify_noalloc.argtypes = _VERIFY_ARGTYPES[:19] + [ctypes.c_void_p]
+        lib.tv_verify_noalloc.restype = ctypes.c_int
         lib.tv_draft_tokens.argtypes = _SAMPLE_ARGTYPES
         lib.tv_draft_tokens.restype = ctypes.c_int
         lib.tv_commit_paths.argtypes = [ctypes.c_int32, ctypes.c_int32] + \
@@ -118,6 +120,19 @@ def tv_verify(batch, num_nodes, vocab, parents, tokens, target_logits, draft_log
                  draft_logits, dtype, temperature, uniforms, mode, accept_len, accepted_node,
                  bonus_token, status, node_state, node_theta, p_init, counters, workspace,
                  workspace_bytes, stream)
+
+
+def tv_verify_noalloc(batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits,
+                      dtype, temperature, uniforms, mode, accept_len, accepted_node, bonus_token,
+                      status, node_state=None, node_theta=None, p_init=None, counters=None,
+                      stream=None) -> int:
+    """C-ABI ``tv_verify_noalloc``: ``tv_verify`` on the library's own device
+    scratch (no workspace argument); returns the status."""
+    fn = load_library().tv_verify_noalloc
+    return int(fn(batch, num_nodes, vocab, _ptr(parents), _ptr(tokens), _ptr(target_logits),
+                  _ptr(draft_logits), dtype, float(temperature), _ptr(uniforms), mode,
+                  _ptr(accept_len), _ptr(accepted_node), _ptr(bonus_token), _ptr(status),
+                  _ptr(node_state), _ptr(node_theta), _ptr(p_init), _ptr(counters), stream))
 
 
 def tv_verify_tokenlevel(batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits,

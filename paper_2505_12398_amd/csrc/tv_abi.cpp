@@ -125,6 +125,27 @@ int tv_verify_tokenlevel(int32_t batch, int32_t num_nodes, int32_t vocab,
                        p_init, counters, workspace, workspace_bytes, stream);
 }
 
+int tv_verify_noalloc(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
+                      const int32_t* tokens, const void* target_logits,
+                      const void* draft_logits, int32_t dtype, float temperature,
+                      const float* uniforms, int32_t mode, int32_t* accept_len,
+                      int32_t* accepted_node, int32_t* bonus_token, int32_t* status,
+                      int8_t* node_state, float* node_theta, float* p_init, int32_t* counters,
+                      hipStream_t stream) {
+  const tv::VerifyArgs a{batch,       num_nodes,  vocab,  parents,  tokens,     target_logits,
+                         draft_logits, dtype,      temperature, uniforms, mode,  accept_len,
+                         accepted_node, bonus_token, status, node_state, node_theta, p_init,
+                         counters};
+  const int st = tv::validate_args(a);
+  if (st != TV_OK || batch == 0) return st;
+  if (tv::workspace_layout(batch, vocab).bytes > tv::kStaticScratchBytes) return TV_ERR_UNSUPPORTED;
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  const int sst = tv::static_scratch(&scratch, &scratch_bytes);
+  if (sst != TV_OK) return sst;
+  return tv::launch(a, tv::Algo::kTraversal, scratch, stream);
+}
+
 int tv_draft_tokens(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
                     const void* draft_logits, int32_t dtype, float temperature,
                     const float* uniforms, int32_t mode, int32_t* tokens, int32_t* status,

@@ -2635,7 +2635,30 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
 
 }  // namespace tv
 
+// Device scratch of tv_verify_noalloc: the workspace of its calls, one copy on
+// every device the library runs on, held until the process ends. Host code
+// never uses this name as a device address: static_scratch looks up each
+// device's address once and every launch passes that address.
+static __device__ __align__(256) uint8_t scratch[tv::kStaticScratchBytes];
+
 namespace tv {
+
+int static_scratch(void** ptr, size_t* bytes) {
+  constexpr int kMaxDevices = 64;
+  static void* addr[kMaxDevices];
+  static std::mutex mu;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TV_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TV_ERR_HIP;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kStaticScratchBytes;
+  return TV_OK;
+}
 
 int launch_sample(const SampleArgs& a, hipStream_t stream) {
   SampleParams S{a.parents, a.draft, a.uniforms, a.tokens, a.status,

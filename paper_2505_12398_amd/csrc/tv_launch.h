@@ -75,6 +75,14 @@ inline WorkspaceLayout workspace_layout(int32_t batch, int32_t vocab) {
 int validate_args(const VerifyArgs& a);
 int validate(const VerifyArgs& a, void* workspace, size_t workspace_bytes);
 
+// Bytes of the library's own device scratch (tv_verify_noalloc): more than the
+// largest workspace any valid size needs (workspace_layout(TV_MAX_BATCH, .)).
+constexpr size_t kStaticScratchBytes = size_t{3} << 20;
+
+// This device's copy of the library's device scratch, its address looked up
+// once per device with that device current. Returns a tv_status_t.
+int static_scratch(void** ptr, size_t* bytes);
+
 struct SampleArgs {
   int32_t batch;
   int32_t num_nodes;

@@ -205,3 +205,44 @@ def test_commit_argument_errors_launch_nothing(kw, want):
 
 def test_commit_empty_batch_is_ok():
     assert call_commit(batch=0, parents=None, tokens=None) == tv.TV_OK
+
+
+def call_noalloc(**kw):
+    args = dict(batch=2, num_nodes=5, vocab=100, parents=A, tokens=A, target_logits=A,
+                draft_logits=A + 0x1000, dtype=tv.TV_DTYPE_BF16, temperature=1.0, uniforms=A,
+                mode=0, accept_len=A, accepted_node=A, bonus_token=A, status=A)
+    args.update(kw)
+    return tv.tv_verify_noalloc(**args)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(batch=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(num_nodes=0), tv.TV_ERR_INVALID_ARG),
+    (dict(vocab=1), tv.TV_ERR_INVALID_ARG),
+    (dict(dtype=7), tv.TV_ERR_INVALID_ARG),
+    (dict(mode=2), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=float("nan")), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=1e-5), tv.TV_ERR_UNSUPPORTED),
+    (dict(num_nodes=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(batch=tv.TV_MAX_BATCH + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(parents=None), tv.TV_ERR_INVALID_ARG),
+    (dict(status=None), tv.TV_ERR_INVALID_ARG),
+    (dict(target_logits=A + 2, draft_logits=A + 4), tv.TV_ERR_UNSUPPORTED),
+    (dict(counters=A + 1), tv.TV_ERR_INVALID_ARG),
+])
+def test_noalloc_argument_errors_launch_nothing(kw, want):
+    """tv_verify_noalloc checks its arguments on the host before it looks up
+    its device scratch (no GPU here)."""
+    assert call_noalloc(**kw) == want
+
+
+def test_noalloc_empty_batch_is_ok():
+    assert call_noalloc(batch=0, parents=None, tokens=None, target_logits=None,
+                        draft_logits=None, uniforms=None, accept_len=None, accepted_node=None,
+                        bonus_token=None, status=None) == tv.TV_OK
+
+
+def test_noalloc_scratch_covers_every_valid_size():
+    """The static scratch (3 MiB) holds the workspace of the largest call the
+    limits allow."""
+    assert tv.tv_workspace_size(tv.TV_MAX_BATCH, tv.TV_MAX_NODES, tv.TV_MAX_VOCAB) <= 3 << 20
