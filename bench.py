@@ -130,15 +130,7 @@ def cpu_baseline(batch, gpu_outs: dict, sample: int, workers: int):
         rep = parity.ParityReport()
         for b, ref in enumerate(refs):
             kind, msg, worst = parity.compare_tree(g, b, ref, False, False, "bf16")
-            rep.trees += 1
-            rep.max_theta_rel = max(rep.max_theta_rel, worst[0])
-            rep.max_theta_abs = max(rep.max_theta_abs, worst[1])
-            if kind == "exact":
-                rep.exact += 1
-            elif kind == "near_tie":
-                rep.near_ties += 1
-            else:
-                rep.failures.append(f"{label} tree {b}: {msg}")
+            rep.record(kind, msg, worst, f"{label} tree {b}")
         reps[label] = rep
     return sample / dt, dt, reps
 
@@ -556,19 +548,14 @@ def main():
             with mp.get_context("fork").Pool(workers) as pool:
                 refs = pool.map(_oracle_one, [(t, batch["temperature"], mode) for t in trees])
             for b, ref in enumerate(refs):
-                kind, msg, _ = parity.compare_tree(g, b, ref, False, False, "bf16")
-                tot.trees += 1
-                if kind == "exact":
-                    tot.exact += 1
-                elif kind == "near_tie":
-                    tot.near_ties += 1
-                else:
-                    tot.failures.append(f"step {k} tree {b}: {msg}")
+                kind, msg, worst = parity.compare_tree(g, b, ref, False, False, "bf16")
+                tot.record(kind, msg, worst, f"step {k} tree {b}")
             print(f"parity step {k + 1}/{args.parity_steps}: {tot.summary()}", file=sys.stderr,
                   flush=True)
             del batch, out
         res["parity_steps"] = {"steps": args.parity_steps, "trees": tot.trees,
-                               "exact": tot.exact, "near_ties": tot.near_ties,
+                               "exact": tot.exact, "zero_rate_boundary": tot.zero_rate,
+                               "near_ties": tot.near_ties,
                                "failures": len(tot.failures)}
         if tot.failures:
             print("\n".join(tot.failures[:5]), file=sys.stderr)
@@ -604,7 +591,9 @@ def main():
         rep, rth = reps["timed"], reps["theta"]
         res["parity_sample"] = {"trees": rep.trees, "exact": rep.exact,
                                 "near_ties": rep.near_ties, "failures": len(rep.failures),
+                                "zero_rate_boundary": rep.zero_rate,
                                 "with_theta": {"exact": rth.exact, "near_ties": rth.near_ties,
+                                               "zero_rate_boundary": rth.zero_rate,
                                                "failures": len(rth.failures),
                                                "max_theta_rel_err": rth.max_theta_rel,
                                                "max_theta_abs_err": rth.max_theta_abs}}
