@@ -338,6 +338,151 @@ def config_leg(cfg_id: int, steps: int, tl_steps: int, mode: int, stream, batch=
             "cache": "512 MiB written before each launch (cold rows)"}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
+
+
+def lmhead_leg(steps: int, stream) -> dict:
+    """tv_lmhead_stats at the size of one verification step of the large-batch
+    workload: 16640 rows (256 trees x 65 nodes), hidden 4096 (Llama-3-8B),
+    V = 128256, bf16, T = 1: logits plus their row statistics in one kernel.
+    Roofline: bf16 MFMA FLOPs (2 M N K). Four sampled rows are checked
+    against the oracle (exact products; statistics of the written logits)."""
+    import numpy as np
+    import torch
+
+    import paper_2505_12398_amd as tv
+    import oracle.lmhead as LM
+    dev = torch.device("cuda", 0)
+    M, K, N = 16640, 4096, 128256
+    g = torch.Generator(device=dev).manual_seed(11)
+    x = torch.randn((M, K), generator=g, device=dev).to(torch.bfloat16)
+    w = (torch.randn((N, K), generator=g, device=dev) * (3.0 / K ** 0.5)).to(torch.bfloat16)
+    out = (torch.empty((M, N), dtype=torch.bfloat16, device=dev),
+           torch.empty(M, dtype=torch.float32, device=dev),
+           torch.empty(M, dtype=torch.float64, device=dev))
+    times = []
+    for i in range(steps + 1):
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        tv.lmhead_stats(x, w, 1.0, stream=stream.cuda_stream, out=out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if i:
+            times.append(e0.elapsed_time(e1))
+    ms = sum(times) / len(times)
+    flops = 2.0 * M * N * K
+    tflops = flops / (ms * 1e-3) / 1e12
+    # a library GEMM without the statistics, for context
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    y = x @ w.T
+    e0.record(stream)
+    for _ in range(3):
+        y = x @ w.T
+    e1.record(stream)
+    torch.cuda.synchronize()
+    lib_ms = e0.elapsed_time(e1) / 3
+    del y
+    # parity of sampled rows
+    rows = [0, 4097, 9000, M - 1]
+    def bits(t):
+        return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    xb, wb = bits(x[rows]), bits(w)
+    exact = LM.logits(xb, wb)
+    bound = LM.accumulation_bound(xb, wb)
+    got = bits(out[0][rows])
+    gz = LM.to_f64(got)
+    ok_logits = bool(np.all(np.abs(gz - exact) <= 2.0 ** -8 * np.abs(exact)
+                            + 2.0 * K * 2.0 ** -24 * bound + 1e-30))
+    m, ssum = LM.row_stats(got, 1.0)
+    gm = out[1][rows].cpu().numpy().astype(np.float64)
+    gs = out[2][rows].cpu().numpy()
+    rel = float(np.max(np.abs(gs - ssum) / ssum))
+    del x, w, out
+    torch.cuda.empty_cache()
+    return {"workload": "LM head 16640 rows x hidden 4096 x V 128256 bf16 (one 256-tree step)",
+            "ms_per_step": ms, "tflops": tflops,
+            "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
+                         "kernel": "lmhead_kernel (tv_lmhead_stats)"},
+            "library_gemm_without_statistics": {"ms": lib_ms,
+                                                "tflops": flops / (lib_ms * 1e-3) / 1e12,
+                                                "what": "torch matmul (hipBLASLt), logits only"},
+            "parity_sample": {"rows": len(rows), "logits_within_bound": ok_logits,
+                              "row_max_exact": bool(np.array_equal(gm, m)),
+                              "row_sum_max_rel_err": rel}}
+
+
+def verify_stats_leg(steps: int, mode: int, stream, workers: int) -> dict:
+    """tv_verify_stats on the large-batch workload: the row statistics are given
+    (as an LM head with fused statistics produces them; here computed from the
+    synthetic logits outside the timed region), so the verifier reads rows
+    only for residual updates and Y. Algorithmic bytes: both rows per executed
+    residual update, the accepted leaf's target row, the small per-node data.
+    16 trees of the last step are checked against the oracle."""
+    import torch
+
+    import paper_2505_12398_amd as tv
+    import workloads as W
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity  # noqa: E402  (test infrastructure: oracle comparison)
+    dev = torch.device("cuda", 0)
+    cfg = W.CONFIGS[CFG]
+    B, n1, V = cfg.batch, cfg.n_nodes + 1, cfg.vocab
+    ws, _ = tv.workspace_tensor(B, n1, V, dev)
+
+    def stats_of(z, T):
+        zf = z.double()
+        m = zf.amax(dim=-1)
+        s = torch.exp((zf - m.unsqueeze(-1)) / float(T)).sum(dim=-1)
+        return m.float().contiguous(), s.contiguous()
+
+    times, nbytes, acc = [], [], []
+    last = None
+    for s_ in range(steps + 2):
+        bt = W.make_batch(CFG, step=40_000 + s_, device=dev, mode=mode, seed=3)
+        tm, ts = stats_of(bt["target"], bt["temperature"])
+        dm, ds = stats_of(bt["draft"], bt["temperature"])
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        e0.record(stream)
+        out = tv.verify_batch(bt["parents"], bt["tokens"], bt["target"], bt["draft"],
+                              bt["temperature"], bt["uniforms"], mode, want_nodes=False,
+                              want_counters=True, stream=stream.cuda_stream, workspace=ws,
+                              stats=(tm, ts, dm, ds))
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if s_ >= 2:
+            times.append(e0.elapsed_time(e1))
+            c = out.counters[out.status == 0].sum(dim=0).tolist()
+            row = V * 2
+            nbytes.append(2 * row * c[1] + row * c[2] + B * n1 * 17 + B * 32)
+            acc.append(out.accept_len.float().mean().item() + 1.0)
+            last = (bt, (tm, ts, dm, ds))
+        del bt
+    ms = sum(times) / len(times)
+    alg = sum(nbytes) / len(nbytes)
+    bt, stats = last
+    g = parity.host_outputs(tv.verify_batch(bt["parents"], bt["tokens"], bt["target"],
+                                            bt["draft"], bt["temperature"], bt["uniforms"], mode,
+                                            want_nodes=True, want_theta=False, stats=stats))
+    trees = list(range(0, B, B // 16))
+    refs = parity.oracle_many(bt, trees, tokenlevels=(False,), workers=workers)[False]
+    rep = parity.check(bt, False, trees=trees, refs=refs, gpu=g, theta=False, label="stats")
+    gbps = alg / (ms * 1e-3) / 1e9
+    return {"workload": cfg.name + " with the row statistics given (tv_verify_stats)",
+            "ms_per_step": ms, "trees_per_s": B / (ms * 1e-3),
+            "algorithmic_bytes_per_launch": alg, "achieved_GBps": gbps,
+            "frac": gbps / HBM_PEAK_GBPS, "accept_len_mean": sum(acc) / len(acc),
+            "parity_sample": {"trees": rep.trees, "exact": rep.exact,
+                              "near_ties": rep.near_ties, "failures": len(rep.failures)}}
+
+
 def _oracle_one(args):
     (par, tok, zb, zs, u), T, mode = args
     from oracle import verify_tree
@@ -365,6 +510,10 @@ def main():
     ap.add_argument("--config-steps", type=int, default=10,
                     help="timed launches per smaller workload (chain, binary tree, irregular "
                          "tree) and of the one-tree latency leg (0: skip them)")
+    ap.add_argument("--lmhead-steps", type=int, default=3,
+                    help="timed launches of the LM head with fused statistics (0: skip)")
+    ap.add_argument("--stats-steps", type=int, default=20,
+                    help="timed launches of the verifier with row statistics given (0: skip)")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="only run plain device-to-device copies of this size (to scale "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -528,6 +677,15 @@ def main():
             CFG, 2 * args.config_steps, args.config_steps, mode, stream, batch=1,
             label=cfg.name.replace("B256", "B1") + " (one tree per call: latency)")
         print("single-tree leg done", file=sys.stderr, flush=True)
+
+    if args.stats_steps > 0:
+        res["verify_with_stats"] = verify_stats_leg(args.stats_steps, mode, stream,
+                                                    args.cpu_workers or min(16, os.cpu_count() or 1))
+        print("verify-with-statistics leg done", file=sys.stderr, flush=True)
+
+    if args.lmhead_steps > 0:
+        res["lmhead"] = lmhead_leg(args.lmhead_steps, stream)
+        print("LM-head leg done", file=sys.stderr, flush=True)
 
     if args.sampler_steps > 0 and last is not None:
         res["draft_sampler"] = sampler_leg(last[0], args.sampler_steps, stream, elem)

@@ -127,6 +127,8 @@ enum {
 #define TV_MIN_TEMPERATURE 1.0e-3f
 #define TV_MAX_TEMPERATURE 1.0e3f
 #define TV_NUM_COUNTERS 4
+#define TV_MAX_LMHEAD_ROWS (1 << 24)    /* rows of one tv_lmhead_stats call */
+#define TV_MAX_HIDDEN (1 << 16)         /* hidden size of tv_lmhead_stats */
 
 /*
  * Bytes of device workspace tv_verify / tv_verify_tokenlevel need for these
@@ -207,6 +209,59 @@ int tv_verify_noalloc(int32_t batch, int32_t num_nodes, int32_t vocab,
                       int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
                       int32_t* status, int8_t* node_state, float* node_theta, float* p_init,
                       int32_t* counters, hipStream_t stream);
+
+/*
+ * tv_verify with the row statistics given by the caller, so that the verifier
+ * reads a node's logits only for its residual updates (Eq. e1-e3) and for Y,
+ * never to normalise them. The distributions of the problem statement
+ * (Alg. 3 REQUIRE) are softmax(logits / T) per row; for row (b, i):
+ *   target_max[b][i] = max_x target_logits[b][i][x]          float [batch][num_nodes]
+ *   target_sum[b][i] = sum_x exp((target_logits[b][i][x] - target_max[b][i]) / T)
+ *                                                              double [batch][num_nodes]
+ * and the same for the draft rows (draft_max, draft_sum). tv_lmhead_stats
+ * produces them with the logits; any producer may be used. Only the entries
+ * of nodes that have children are read. A non-finite maximum, or a sum that is
+ * not finite and positive, at a row the traversal consults gives
+ * TV_TREE_NONFINITE. Every other argument, output and status is that of
+ * tv_verify; the results equal tv_verify's up to the rounding of the sums.
+ * All four pointers are required (else TV_ERR_INVALID_ARG).
+ */
+int tv_verify_stats(int32_t batch, int32_t num_nodes, int32_t vocab,
+                    const int32_t* parents, const int32_t* tokens,
+                    const void* target_logits, const void* draft_logits, int32_t dtype,
+                    float temperature, const float* uniforms, int32_t mode,
+                    const float* target_max, const double* target_sum,
+                    const float* draft_max, const double* draft_sum,
+                    int32_t* accept_len, int32_t* accepted_node, int32_t* bonus_token,
+                    int32_t* status, int8_t* node_state, float* node_theta, float* p_init,
+                    int32_t* counters, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
+
+/*
+ * LM head with fused row statistics: the model layer whose outputs the
+ * verifier reads. For rows = the tree nodes of a batch (M), hidden size K and
+ * vocabulary N:
+ *   logits[m][n] = bf16( sum_k hidden[m][k] * weight[n][k] )   (fp32 accumulation,
+ *                                                              round to nearest even)
+ *   row_max[m]   = max_n logits[m][n]
+ *   row_sum[m]   = sum_n exp((logits[m][n] - row_max[m]) / T)  (of the rounded logits)
+ * which are the inputs tv_verify_stats takes (one call for the target model,
+ * one for the draft model). hidden bf16 [rows][hidden_size], weight bf16
+ * [vocab][hidden_size] (the usual [out][in] layout of a linear layer), both
+ * 16-byte aligned and contiguous, hidden_size a multiple of 8; logits bf16
+ * [rows][vocab]; row_max float [rows]; row_sum double [rows]. The matrix
+ * products run on the bf16 matrix cores (MFMA); the statistics are formed in
+ * the same kernel from the rounded logits it holds, so they cost no pass over
+ * the logits. A NaN or infinite logit makes its row's sum NaN or infinite.
+ * workspace: device buffer of tv_lmhead_workspace_size(rows, vocab) bytes,
+ * 256-byte aligned (per-tile partial statistics). Returns a tv_status_t;
+ * argument errors launch nothing.
+ */
+size_t tv_lmhead_workspace_size(int32_t rows, int32_t vocab);
+int tv_lmhead_stats(int32_t rows, int32_t hidden_size, int32_t vocab, const void* hidden,
+                    const void* weight, float temperature, void* logits, float* row_max,
+                    double* row_sum, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
 
 /*
  * Token-level tree verification (Sec. 2.2): starting at the root, the children

@@ -16,6 +16,9 @@ Contents:
 * :mod:`oracle.draft_sampler` -- the tokens of a draft tree drawn from each
   parent's tempered draft distribution, with or without replacement
   (Def. de_tree, Sec. 3.3), by inverse CDF at given uniforms.
+* :mod:`oracle.lmhead` -- an LM head's logits (the exact product of bf16
+  hidden states and output embeddings) and every row's maximum and sum of
+  exp((z - max) / T), the normalisers of the per-node distributions.
 
 Pins (what the oracle is checked against, independent of itself) live in
 ``tests/oracle_pins.py`` (run by ``tests/test_oracle_pins.py``) and

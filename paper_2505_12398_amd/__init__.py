@@ -18,5 +18,6 @@ from ._lib import (  # noqa: F401
     LIB_PATH, TvError, load_library,
     tv_workspace_size, tv_verify, tv_verify_noalloc, tv_verify_tokenlevel, tv_status_string, tv_draft_tokens,
     draft_tokens, tv_commit_paths, commit_paths, TV_COMMIT_OVERFLOW, TV_COMMIT_INCONSISTENT,
-    VerifyOutputs, verify_batch, workspace_tensor,
+    VerifyOutputs, verify_batch, workspace_tensor, tv_verify_stats, tv_lmhead_workspace_size,
+    tv_lmhead_stats, lmhead_stats, TV_MAX_LMHEAD_ROWS, TV_MAX_HIDDEN,
 )

@@ -19,6 +19,8 @@ TV_MAX_NODES = 1024
 TV_MAX_VOCAB = 1 << 20
 TV_MAX_VOCAB_F32 = 1 << 19
 TV_NUM_COUNTERS = 4
+TV_MAX_LMHEAD_ROWS = 1 << 24
+TV_MAX_HIDDEN = 1 << 16
 
 
 class TvError(RuntimeError):
@@ -64,6 +66,14 @@ def load_library(path: str = LIB_PATH):
             fn.restype = ctypes.c_int
         lib.tv_verify_noalloc.argtypes = _VERIFY_ARGTYPES[:19] + [ctypes.c_void_p]
         lib.tv_verify_noalloc.restype = ctypes.c_int
+        lib.tv_verify_stats.argtypes = (_VERIFY_ARGTYPES[:11] + [ctypes.c_void_p] * 4 +
+                                        _VERIFY_ARGTYPES[11:])
+        lib.tv_verify_stats.restype = ctypes.c_int
+        lib.tv_lmhead_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32]
+        lib.tv_lmhead_workspace_size.restype = ctypes.c_size_t
+        lib.tv_lmhead_stats.argtypes = [ctypes.c_int32] * 3 + [ctypes.c_void_p] * 2 + \
+            [ctypes.c_float] + [ctypes.c_void_p] * 4 + [ctypes.c_size_t, ctypes.c_void_p]
+        lib.tv_lmhead_stats.restype = ctypes.c_int
         lib.tv_draft_tokens.argtypes = _SAMPLE_ARGTYPES
         lib.tv_draft_tokens.restype = ctypes.c_int
         lib.tv_commit_paths.argtypes = [ctypes.c_int32, ctypes.c_int32] + \
@@ -133,6 +143,65 @@ def tv_verify_noalloc(batch, num_nodes, vocab, parents, tokens, target_logits, d
                   _ptr(draft_logits), dtype, float(temperature), _ptr(uniforms), mode,
                   _ptr(accept_len), _ptr(accepted_node), _ptr(bonus_token), _ptr(status),
                   _ptr(node_state), _ptr(node_theta), _ptr(p_init), _ptr(counters), stream))
+
+
+def tv_verify_stats(batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits,
+                    dtype, temperature, uniforms, mode, target_max, target_sum, draft_max,
+                    draft_sum, accept_len, accepted_node, bonus_token, status, node_state=None,
+                    node_theta=None, p_init=None, counters=None, workspace=None,
+                    workspace_bytes=0, stream=None) -> int:
+    """C-ABI ``tv_verify_stats``: ``tv_verify`` with the row statistics given."""
+    fn = load_library().tv_verify_stats
+    return int(fn(batch, num_nodes, vocab, _ptr(parents), _ptr(tokens), _ptr(target_logits),
+                  _ptr(draft_logits), dtype, float(temperature), _ptr(uniforms), mode,
+                  _ptr(target_max), _ptr(target_sum), _ptr(draft_max), _ptr(draft_sum),
+                  _ptr(accept_len), _ptr(accepted_node), _ptr(bonus_token), _ptr(status),
+                  _ptr(node_state), _ptr(node_theta), _ptr(p_init), _ptr(counters),
+                  _ptr(workspace), int(workspace_bytes), stream))
+
+
+def tv_lmhead_workspace_size(rows: int, vocab: int) -> int:
+    return int(load_library().tv_lmhead_workspace_size(rows, vocab))
+
+
+def tv_lmhead_stats(rows, hidden_size, vocab, hidden, weight, temperature, logits, row_max,
+                    row_sum, workspace, workspace_bytes, stream=None) -> int:
+    """C-ABI ``tv_lmhead_stats``: pointers may be torch tensors or raw ints."""
+    return int(load_library().tv_lmhead_stats(
+        int(rows), int(hidden_size), int(vocab), _ptr(hidden), _ptr(weight), float(temperature),
+        _ptr(logits), _ptr(row_max), _ptr(row_sum), _ptr(workspace), int(workspace_bytes),
+        _ptr(stream)))
+
+
+def lmhead_stats(hidden, weight, temperature, stream=None, out=None):
+    """Logits and their row statistics for bf16 hidden states [..., K] and a bf16
+    weight [N, K] (torch tensors on one device); returns (logits [..., N] bf16,
+    row_max [...] float32, row_sum [...] float64). Raises on a non-OK return."""
+    import torch
+    K = hidden.shape[-1]
+    N = weight.shape[0]
+    lead = tuple(hidden.shape[:-1])
+    M = 1
+    for d in lead:
+        M *= d
+    dev = hidden.device
+    if hidden.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16:
+        raise TypeError("hidden and weight must be bfloat16")
+    if tuple(weight.shape) != (N, K) or not hidden.is_contiguous() or not weight.is_contiguous():
+        raise ValueError("weight must be [vocab, hidden] and both tensors contiguous")
+    if out is None:
+        out = (torch.empty(lead + (N,), dtype=torch.bfloat16, device=dev),
+               torch.empty(lead, dtype=torch.float32, device=dev),
+               torch.empty(lead, dtype=torch.float64, device=dev))
+    nbytes = tv_lmhead_workspace_size(M, N)
+    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream if dev.type == "cuda" else None
+    st = tv_lmhead_stats(M, K, N, hidden, weight, temperature, out[0], out[1], out[2], ws, nbytes,
+                         stream)
+    if st != TV_OK:
+        raise TvError(st, "tv_lmhead_stats")
+    return out
 
 
 def tv_verify_tokenlevel(batch, num_nodes, vocab, parents, tokens, target_logits, draft_logits,
@@ -237,12 +306,14 @@ class VerifyOutputs:
 def verify_batch(parents, tokens, target_logits, draft_logits, temperature, uniforms, mode,
                  tokenlevel=False, want_nodes=True, want_p_init=False, want_counters=True,
                  out: VerifyOutputs | None = None, stream=None,
-                 workspace=None, want_theta=None) -> VerifyOutputs:
+                 workspace=None, want_theta=None, stats=None) -> VerifyOutputs:
     """Allocate outputs and the workspace (torch, same device) unless given,
     check shapes, call the C entry point on the current stream and raise on a
     non-OK return. ``want_nodes`` asks for node states and (unless
     ``want_theta`` is False) the tested probabilities; without the latter,
-    tv_verify skips the residual updates that decide nothing."""
+    tv_verify skips the residual updates that decide nothing. ``stats`` =
+    (target_max, target_sum, draft_max, draft_sum) [B, N+1] tensors calls
+    tv_verify_stats (Traversal Verification with the row statistics given)."""
     import torch
     B, n1 = parents.shape
     V = target_logits.shape[-1]
@@ -278,6 +349,22 @@ def verify_batch(parents, tokens, target_logits, draft_logits, temperature, unif
         workspace, ws_bytes = workspace_tensor(B, n1, V, dev)
     else:
         ws_bytes = workspace.numel() * workspace.element_size()
+    if stats is not None:
+        if tokenlevel:
+            raise ValueError("row statistics are taken by Traversal Verification only")
+        tm, ts, dm, ds = stats
+        for name, t, dt in (("target_max", tm, torch.float32), ("target_sum", ts, torch.float64),
+                            ("draft_max", dm, torch.float32), ("draft_sum", ds, torch.float64)):
+            if tuple(t.shape) != (B, n1) or t.dtype != dt or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous {dt} tensor of shape {(B, n1)}")
+        st = tv_verify_stats(B, n1, V, parents, tokens, target_logits, draft_logits, dtype,
+                             temperature, uniforms, mode, tm, ts, dm, ds, out.accept_len,
+                             out.accepted_node, out.bonus_token, out.status, out.node_state,
+                             out.node_theta, out.p_init, out.counters, workspace, ws_bytes,
+                             stream)
+        if st != TV_OK:
+            raise TvError(st, "tv_verify_stats")
+        return out
     fn = tv_verify_tokenlevel if tokenlevel else tv_verify
     st = fn(B, n1, V, parents, tokens, target_logits, draft_logits, dtype, temperature,
             uniforms, mode, out.accept_len, out.accepted_node, out.bonus_token, out.status,

@@ -10,7 +10,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libtv.so")
 
-SOURCES = ["tv_abi.cpp", "tv_kernels.hip", "tv_commit.hip"]
+SOURCES = ["tv_abi.cpp", "tv_kernels.hip", "tv_commit.hip", "tv_lmhead.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -46,6 +46,26 @@ int validate_args(const VerifyArgs& a) {
   return TV_OK;
 }
 
+int validate_lmhead(const LmheadArgs& a, void* workspace, size_t workspace_bytes) {
+  if (a.rows < 0 || a.hidden_size < 8 || a.vocab < 2) return TV_ERR_INVALID_ARG;
+  if (a.hidden_size % 8) return TV_ERR_UNSUPPORTED;
+  if (!(a.temperature > 0.0f) || !isfinite(a.temperature)) return TV_ERR_INVALID_ARG;
+  if (a.temperature < TV_MIN_TEMPERATURE || a.temperature > TV_MAX_TEMPERATURE)
+    return TV_ERR_UNSUPPORTED;
+  if (a.rows > TV_MAX_LMHEAD_ROWS || a.hidden_size > TV_MAX_HIDDEN || a.vocab > TV_MAX_VOCAB)
+    return TV_ERR_UNSUPPORTED;
+  if (a.rows == 0) return TV_OK;
+  if (!a.hidden || !a.weight || !a.logits || !a.row_max || !a.row_sum) return TV_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(a.hidden) % 16 || reinterpret_cast<uintptr_t>(a.weight) % 16 ||
+      reinterpret_cast<uintptr_t>(a.logits) % 2 || reinterpret_cast<uintptr_t>(a.row_max) % 4 ||
+      reinterpret_cast<uintptr_t>(a.row_sum) % 8)
+    return TV_ERR_INVALID_ARG;
+  if (!workspace || reinterpret_cast<uintptr_t>(workspace) % 256 ||
+      workspace_bytes < lmhead_layout(a.rows, a.vocab).bytes)
+    return TV_ERR_WORKSPACE;
+  return TV_OK;
+}
+
 int validate_sample(const SampleArgs& a) {
   if (a.batch < 0 || a.num_nodes < 1 || a.vocab < 2) return TV_ERR_INVALID_ARG;
   if (a.dtype != TV_DTYPE_BF16 && a.dtype != TV_DTYPE_F32) return TV_ERR_INVALID_ARG;
@@ -144,6 +164,47 @@ int tv_verify_noalloc(int32_t batch, int32_t num_nodes, int32_t vocab, const int
   const int sst = tv::static_scratch(&scratch, &scratch_bytes);
   if (sst != TV_OK) return sst;
   return tv::launch(a, tv::Algo::kTraversal, scratch, stream);
+}
+
+int tv_verify_stats(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,
+                    const int32_t* tokens, const void* target_logits, const void* draft_logits,
+                    int32_t dtype, float temperature, const float* uniforms, int32_t mode,
+                    const float* target_max, const double* target_sum, const float* draft_max,
+                    const double* draft_sum, int32_t* accept_len, int32_t* accepted_node,
+                    int32_t* bonus_token, int32_t* status, int8_t* node_state, float* node_theta,
+                    float* p_init, int32_t* counters, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+  tv::VerifyArgs a{batch,       num_nodes,  vocab,  parents,  tokens,     target_logits,
+                   draft_logits, dtype,      temperature, uniforms, mode,  accept_len,
+                   accepted_node, bonus_token, status, node_state, node_theta, p_init,
+                   counters};
+  a.target_max = target_max;
+  a.target_sum = target_sum;
+  a.draft_max = draft_max;
+  a.draft_sum = draft_sum;
+  const int st = tv::validate(a, workspace, workspace_bytes);
+  if (st != TV_OK || batch == 0) return st;
+  if (!target_max || !target_sum || !draft_max || !draft_sum) return TV_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(target_max) % 4 || reinterpret_cast<uintptr_t>(draft_max) % 4 ||
+      reinterpret_cast<uintptr_t>(target_sum) % 8 || reinterpret_cast<uintptr_t>(draft_sum) % 8)
+    return TV_ERR_INVALID_ARG;
+  return tv::launch(a, tv::Algo::kTraversal, workspace, stream);
+}
+
+size_t tv_lmhead_workspace_size(int32_t rows, int32_t vocab) {
+  if (rows < 1 || rows > TV_MAX_LMHEAD_ROWS || vocab < 2 || vocab > TV_MAX_VOCAB) return 0;
+  return tv::lmhead_layout(rows, vocab).bytes;
+}
+
+int tv_lmhead_stats(int32_t rows, int32_t hidden_size, int32_t vocab, const void* hidden,
+                    const void* weight, float temperature, void* logits, float* row_max,
+                    double* row_sum, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+  const tv::LmheadArgs a{rows, hidden_size, vocab, hidden, weight, temperature, logits, row_max,
+                         row_sum};
+  const int st = tv::validate_lmhead(a, workspace, workspace_bytes);
+  if (st != TV_OK || rows == 0) return st;
+  return tv::launch_lmhead(a, workspace, stream);
 }
 
 int tv_draft_tokens(int32_t batch, int32_t num_nodes, int32_t vocab, const int32_t* parents,

@@ -113,6 +113,10 @@ struct Params {
   float* node_theta;
   float* p_init;
   int32_t* counters;
+  const float* tmax;         // row statistics given by the caller, or NULL (see tv_verify_stats)
+  const double* tsum;
+  const float* dmax;
+  const double* dsum;
   uint8_t* ws;
   size_t off_parts, parts_words;
   size_t off_desc, desc_words;
@@ -397,6 +401,12 @@ struct FastArith {                 // hardware exp2 of an fp32 fma
   static constexpr bool kPrecise = false;
   float k;                         // log2(e) / T rounded to fp32
   __device__ double frame(float m) const { return static_cast<double>(-m * k); }
+  // 2^(frame(m) + m k): the rounding of the fp32 product in frame(m). A row
+  // sum given in the exact frame of its maximum times this is the sum of the
+  // terms 2^(z k + frame(m)) this arithmetic forms.
+  __device__ double frame_rounding(float m) const {
+    return exp2(frame(m) + static_cast<double>(m) * static_cast<double>(k));
+  }
   __device__ double ex(float z, double c) const {
     return static_cast<double>(fast_exp2(fmaf(z, k, static_cast<float>(c))));
   }
@@ -407,6 +417,7 @@ struct PreciseArith {              // fp64 throughout
   static constexpr bool kPrecise = true;
   double k;                        // log2(e) / T
   __device__ double frame(float m) const { return -static_cast<double>(m) * k; }
+  __device__ double frame_rounding(float) const { return 1.0; }
   __device__ double ex(float z, double c) const {
     return exp2(fma(static_cast<double>(z), k, c));
   }
@@ -1139,9 +1150,9 @@ __device__ __forceinline__ const T* row_ptr(const PP& P, const void* base, int b
 
 // Loads and checks tree b into LDS, gathers every node's logits at its token
 // in its parent's rows, and starts the traversal (all threads).
-template <typename T, int kCap>
+template <typename T, class A, int kCap>
 __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, const Lds<Params>& P,
-                                                     int b) {
+                                                     A ar, int b) {
   const int tid = threadIdx.x;
   const int n1 = P.num_nodes;
   const int V = P.vocab;
@@ -1213,6 +1224,26 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, co
       const int j = sm.parent[i], x = sm.token[i];
       sm.gb[i] = Elem<T>::scalar(row_ptr<T>(P, P.target, b, j) + x);
       sm.gs[i] = Elem<T>::scalar(row_ptr<T>(P, P.draft, b, j) + x);
+    }
+    if (P.tmax) {
+      // Row statistics given by the caller: every node with children has its
+      // STATS results (the frame of its maximum and the inverse of its sum),
+      // so the traversal issues no STATS pass; then every child's ratio.
+      for (int j = tid; j < n1; j += kNT) {
+        if (sm.child_count[j] == 0) continue;
+        const float mb = P.tmax[tree_off + j], ms = P.dmax[tree_off + j];
+        const double tb = P.tsum[tree_off + j], ts = P.dsum[tree_off + j];
+        const bool bad = !(mb > -INFINITY) || !isfinite(mb) || !(ms > -INFINITY) ||
+                         !isfinite(ms) || !(tb > 0.0) || !isfinite(tb) || !(ts > 0.0) ||
+                         !isfinite(ts);
+        sm.cb[j] = ar.frame(bad ? 0.0f : mb);
+        sm.cs[j] = ar.frame(bad ? 0.0f : ms);
+        sm.invsb[j] = bad ? 1.0 : 1.0 / (tb * ar.frame_rounding(mb));
+        sm.invss[j] = bad ? 1.0 : 1.0 / (ts * ar.frame_rounding(ms));
+        sm.flags[j] |= kFlagStats | (bad ? kFlagBad : 0);
+      }
+      __syncthreads();
+      for (int c = 1 + tid; c < n1; c += kNT) child_ratio(sm, ar, sm.parent[c], c);
     }
   }
   if (tid == 0) {
@@ -1316,6 +1347,21 @@ __device__ __forceinline__ bool await_part(const PP& P, const SegPart* part, int
   }
 }
 
+// Child c's original ratio r0 = p(x)/q(x) at its parent j and its draft term,
+// from j's row statistics and the gathered logits; a drafted token the draft
+// cannot produce (draft logit -inf) marks j bad.
+template <class A, int kCap>
+__device__ __forceinline__ void child_ratio(Lds<TreeSmem<kCap>>& sm, const A& ar, int j, int c) {
+  const double kd = ar.kd();
+  const double Cb = sm.cb[j], Cs = sm.cs[j];
+  const double norm = sm.invsb[j] / sm.invss[j];   // ts / tb
+  const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb);
+  const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs);
+  sm.r0[c] = exp2(lp - lq) * norm;
+  sm.et[c] = ar.ex(sm.gs[c], Cs);
+  if (sm.gs[c] == -INFINITY) sm.flags[j] |= kFlagBad;
+}
+
 // Combines the members' partials of the completed batch (all threads): wave w
 // waits for and takes passes w, w + 4, lanes are members; STATS results go to
 // the node arrays, a SPASS / WSUM result to res_S / res_sd. Returns false if
@@ -1390,22 +1436,13 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
   // children's original ratios r0 = p(x)/q(x) and draft terms: 32 threads per
   // pass (a node with bad statistics gets values it never uses: the traversal
   // fails the tree before it reads them)
-  const double kd = ar.kd();
   static_assert(kMaxBatch * 32 <= kNT, "one thread group of 32 per pass");
   if (tid < bn * 32) {
     const int p = tid >> 5;
     const int node = sm.bnode[p];
-    const bool stats2 = sm.bcmd[p] == kCmdStats2;
-    const double Cb = sm.cb[node], Cs = sm.cs[node];
-    const double norm = sm.invsb[node] / sm.invss[node];   // ts / tb
-    for (int i = tid & 31; stats2 && i < sm.child_count[node]; i += 32) {
-      const int c = sm.child_list[sm.child_start[node] + i];
-      const double lp = fma(static_cast<double>(sm.gb[c]), kd, Cb);
-      const double lq = fma(static_cast<double>(sm.gs[c]), kd, Cs);
-      sm.r0[c] = exp2(lp - lq) * norm;
-      sm.et[c] = ar.ex(sm.gs[c], Cs);
-      if (sm.gs[c] == -INFINITY) sm.flags[node] |= kFlagBad;   // a token the draft cannot produce
-    }
+    if (sm.bcmd[p] == kCmdStats2)
+      for (int i = tid & 31; i < sm.child_count[node]; i += 32)
+        child_ratio(sm, ar, node, sm.child_list[sm.child_start[node] + i]);
   }
   __syncthreads();
   return true;
@@ -1975,12 +2012,13 @@ __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
   const uint32_t seq = sm.seq + 1u;
   const int b = sm.tree;
   const int geff = sm.geff;
-  uint64_t hnext = 0;
+  // Member 0 reads the group's helper count here and uses it only after the
+  // stripes: the load completes under the stripes' own loads instead of
+  // delaying them by a round trip.
+  uint32_t hcount = 0;
   if (m == 0 && tid == 0) {
     if (geff > P.G) publish_batch(P, g, seq, sm, geff);
-    const int n = static_cast<int>(ld_rlx(ws_hcount(P, g)));
-    const int cap = P.Gx - P.G;
-    hnext = static_cast<uint64_t>(n < cap ? n : cap);
+    hcount = ld_rlx(ws_hcount(P, g));
   }
   const TermParams tp{sm.cmd_cb, sm.cmd_cs, sm.cmd_ap, sm.cmd_bp};
   for (int p = 0; p < bn; ++p) {
@@ -1998,7 +2036,10 @@ __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     }
   }
   if (tid == 0) {
-    ws.res_count = hnext;      // the partials are written by the next controller step
+    const int cap = P.Gx - P.G;
+    const int n = static_cast<int>(hcount);
+    ws.res_count = m == 0 ? static_cast<uint64_t>(n < cap ? n : cap) : 0;
+    // the partials are written by the next controller step
     sm.seq = seq;
     sm.pending = 1;
     // the weights of pass 0 stay available for drawing Y at its node
@@ -2069,7 +2110,7 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   __syncthreads();
   bool live = true;
   for (int b = g; b < P.batch; b += P.ngroups) {
-    begin_tree<T>(sm, Ps, b);
+    begin_tree<T>(sm, Ps, ar, b);
     for (;;) {
       controller_step<T, A>(sm, ws, Ps, ar, g, m, false);
       while (sm.cmd == kCmdLocalSample) {
@@ -2611,6 +2652,10 @@ int launch(const VerifyArgs& a, Algo algo, void* workspace, hipStream_t stream) 
   P.node_theta = a.node_theta;
   P.p_init = a.p_init;
   P.counters = a.counters;
+  P.tmax = a.target_max;
+  P.tsum = a.target_sum;
+  P.dmax = a.draft_max;
+  P.dsum = a.draft_sum;
   P.ws = static_cast<uint8_t*>(workspace);
   P.off_parts = L.off_parts;
   P.parts_words = L.parts_bytes / 8;

@@ -31,6 +31,12 @@ struct VerifyArgs {
   float* node_theta;
   float* p_init;
   int32_t* counters;
+  // Row statistics given by the caller (tv_verify_stats), [batch][num_nodes]
+  // each, or all NULL: the maximum of the row and sum exp((z - max) / T).
+  const float* target_max = nullptr;
+  const double* target_sum = nullptr;
+  const float* draft_max = nullptr;
+  const double* draft_sum = nullptr;
 };
 
 constexpr int kMaxGrid = 4096;        // workgroups of one launch
@@ -82,6 +88,42 @@ constexpr size_t kStaticScratchBytes = size_t{3} << 20;
 // This device's copy of the library's device scratch, its address looked up
 // once per device with that device current. Returns a tv_status_t.
 int static_scratch(void** ptr, size_t* bytes);
+
+// LM head with fused row statistics (tv_lmhead_stats).
+struct LmheadArgs {
+  int32_t rows;           // M
+  int32_t hidden_size;    // K
+  int32_t vocab;          // N
+  const void* hidden;     // bf16 [M][K]
+  const void* weight;     // bf16 [N][K]
+  float temperature;
+  void* logits;           // bf16 [M][N]
+  float* row_max;         // [M]
+  double* row_sum;        // [M]
+};
+
+constexpr int kLmheadTileN = 128;   // logits columns per workgroup
+
+// Workspace of tv_lmhead_stats: one (max, sum) partial per row and column tile.
+struct LmheadLayout {
+  int tiles_n;
+  size_t off_max, off_sum, bytes;
+};
+inline LmheadLayout lmhead_layout(int32_t rows, int32_t vocab) {
+  LmheadLayout L{};
+  L.tiles_n = (vocab + kLmheadTileN - 1) / kLmheadTileN;
+  const size_t n = static_cast<size_t>(rows) * static_cast<size_t>(L.tiles_n) * sizeof(float);
+  L.off_max = 0;
+  L.off_sum = align256(n);
+  L.bytes = align256(L.off_sum + n);
+  return L;
+}
+
+// Argument checks of the LM head that need no GPU. Returns a tv_status_t.
+int validate_lmhead(const LmheadArgs& a, void* workspace, size_t workspace_bytes);
+
+// Enqueue the LM head and the merge of its row statistics (arguments validated).
+int launch_lmhead(const LmheadArgs& a, void* workspace, hipStream_t stream);
 
 struct SampleArgs {
   int32_t batch;

@@ -17,6 +17,7 @@ namespace tv {
 int launch(const VerifyArgs&, Algo, void*, hipStream_t) { ++g_launches; return TV_OK; }
 int launch_sample(const SampleArgs&, hipStream_t) { ++g_launches; return TV_OK; }
 int launch_commit(const CommitArgs&, hipStream_t) { ++g_launches; return TV_OK; }
+int launch_lmhead(const LmheadArgs&, void*, hipStream_t) { ++g_launches; return TV_OK; }
 int static_scratch(void** ptr, size_t* bytes) {
   static unsigned char fake[256] __attribute__((aligned(256)));
   *ptr = fake;
@@ -106,6 +107,28 @@ int main() {
   EXPECT(tv_commit_paths(2, 5, ip, ip, ip, ip, ip, 4, nullptr, ip, ip, nullptr) == TV_ERR_INVALID_ARG);
   EXPECT(tv_commit_paths(2, 5, ip, ip, ip, ip, ip, 0, nullptr, ip, ip, nullptr) == TV_OK);
   EXPECT(g_launches == before + 2);
+
+  before = g_launches;
+  const float* fm = reinterpret_cast<const float*>(A);
+  const double* dm = reinterpret_cast<const double*>(A);
+  EXPECT(tv_verify_stats(2, 5, 100, ip, ip, tgt, drf, TV_DTYPE_BF16, 1.0f, fp, 0, fm, dm, fm, dm,
+                         ip, ip, ip, ip, nullptr, nullptr, nullptr, nullptr, ws, wsb, nullptr) ==
+         TV_OK);
+  EXPECT(tv_verify_stats(2, 5, 100, ip, ip, tgt, drf, TV_DTYPE_BF16, 1.0f, fp, 0, nullptr, dm, fm,
+                         dm, ip, ip, ip, ip, nullptr, nullptr, nullptr, nullptr, ws, wsb,
+                         nullptr) == TV_ERR_INVALID_ARG);
+  EXPECT(g_launches == before + 1);
+  before = g_launches;
+  const size_t lwb = tv_lmhead_workspace_size(4, 1000);
+  EXPECT(lwb > 0 && lwb % 256 == 0);
+  double* dp = reinterpret_cast<double*>(A);
+  EXPECT(tv_lmhead_stats(4, 64, 1000, tgt, drf, 1.0f, reinterpret_cast<void*>(A), fp, dp, ws, lwb,
+                         nullptr) == TV_OK);
+  EXPECT(tv_lmhead_stats(4, 60, 1000, tgt, drf, 1.0f, reinterpret_cast<void*>(A), fp, dp, ws, lwb,
+                         nullptr) == TV_ERR_UNSUPPORTED);
+  EXPECT(tv_lmhead_stats(4, 64, 1000, tgt, drf, 1.0f, reinterpret_cast<void*>(A), fp, dp, ws, 16,
+                         nullptr) == TV_ERR_WORKSPACE);
+  EXPECT(g_launches == before + 1);
 
   for (int c = -3; c < 8; ++c) EXPECT(tv_status_string(c) != nullptr);
   if (failures) {

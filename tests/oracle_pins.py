@@ -19,6 +19,7 @@ import numpy as np
 import oracle.tv_oracle as O
 import oracle.enumerate as E
 import oracle.draft_sampler as DS
+import oracle.lmhead as LM
 import workloads as W
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
@@ -578,13 +579,74 @@ def pin_verifier_statuses():
     assert r.status == O.TREE_NONFINITE
 
 
+# ---------------------------------------------------------------------------
+# LM head and row statistics (the inputs' normalisers)
+# ---------------------------------------------------------------------------
+
+def _bf16_bits(a):
+    a = np.asarray(a, dtype=np.float32)
+    return (a.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def pin_lmhead_logits():
+    """The logits of bf16 inputs against a brute-force triple loop on a small
+    case whose products and sums are exact (small integers and halves), the
+    weight read as [vocab][hidden]; and every exact logit within the
+    accumulation bound's own magnitude."""
+    rng = np.random.default_rng(31)
+    M, K, N = 5, 12, 7
+    x = rng.integers(-4, 5, (M, K)) / 2.0
+    w = rng.integers(-4, 5, (N, K)) / 2.0
+    xb, wb = _bf16_bits(x), _bf16_bits(w)
+    z = LM.logits(xb, wb)
+    for m in range(M):
+        for n in range(N):
+            want = 0.0
+            for k in range(K):
+                want += float(x[m][k]) * float(w[n][k])
+            assert z[m][n] == want, (m, n, z[m][n], want)
+    bound = LM.accumulation_bound(xb, wb)
+    assert np.all(np.abs(z) <= bound) and bound.shape == (M, N)
+
+
+def pin_row_stats():
+    """Row maximum and sum exp((z - max) / T) against scipy's logsumexp
+    (log(sum) + max / T = logsumexp(z / T)), the softmax identity (the
+    normalised terms sum to 1), the temperature's scaling, and the special
+    rows: all -inf gives (-inf, 0), a NaN or +inf gives a non-finite sum."""
+    from scipy.special import logsumexp
+    rng = np.random.default_rng(32)
+    z = rng.normal(0, 3, (6, 50))
+    z[2, 7] = -np.inf
+    for T in (0.2, 0.7, 1.0, 1.9):
+        Tf = float(np.float32(T))
+        m, s = LM.row_stats(z, T)
+        assert np.array_equal(m, z.max(axis=1))
+        np.testing.assert_allclose(np.log(s) + m / Tf, logsumexp(z / Tf, axis=1), rtol=0,
+                                   atol=1e-12)
+        p = np.exp((z - m[:, None]) / Tf) / s[:, None]
+        np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-12)
+    m, s = LM.row_stats(2.0 * z, 2.0)
+    np.testing.assert_allclose(m, 2.0 * z.max(axis=1), atol=0)
+    np.testing.assert_allclose(s, np.exp(z - z.max(axis=1, keepdims=True)).sum(axis=1),
+                               rtol=1e-13)
+    special = np.array([[-np.inf, -np.inf, -np.inf], [0.0, np.nan, 1.0], [0.0, np.inf, 1.0]])
+    m, s = LM.row_stats(special, 1.0)
+    assert m[0] == -np.inf and s[0] == 0.0
+    assert not np.isfinite(s[1]) and not np.isfinite(s[2])
+    # bf16 bit patterns are widened exactly first
+    zb = _bf16_bits(z[:, :8])
+    m2, _ = LM.row_stats(zb, 1.0)
+    assert np.array_equal(m2, O.to_f64(zb).max(axis=1))
+
+
 FAST_PINS = [pin_worked_example_trace, pin_worked_example_tokenlevel, pin_worked_example_law,
              pin_single_token_table1, pin_rrsw_example, pin_tempered_softmax_inverse,
              pin_inverse_cdf_law, pin_identical_models, pin_depth1_equals_rrsw,
              pin_invariants, pin_early_rejection_worked_example, pin_early_rejection_sound,
              pin_draft_sampler_law, pin_draft_sampler_statuses, pin_committed_sequence,
              pin_counters_worked_example, pin_counters_identical_models, pin_bf16_widening,
-             pin_verifier_statuses]
+             pin_verifier_statuses, pin_lmhead_logits, pin_row_stats]
 ENUM_PINS = [pin_lossless_exact, pin_lossless_irregular_T07, pin_chain_optimality]
 ALL_PINS = FAST_PINS + ENUM_PINS
 

@@ -246,3 +246,81 @@ def test_noalloc_scratch_covers_every_valid_size():
     """The static scratch (3 MiB) holds the workspace of the largest call the
     limits allow."""
     assert tv.tv_workspace_size(tv.TV_MAX_BATCH, tv.TV_MAX_NODES, tv.TV_MAX_VOCAB) <= 3 << 20
+
+
+def call_stats(**kw):
+    args = dict(batch=2, num_nodes=5, vocab=100, parents=A, tokens=A, target_logits=A,
+                draft_logits=A + 0x1000, dtype=tv.TV_DTYPE_BF16, temperature=1.0, uniforms=A,
+                mode=0, target_max=A, target_sum=A, draft_max=A, draft_sum=A, accept_len=A,
+                accepted_node=A, bonus_token=A, status=A, workspace=WS,
+                workspace_bytes=tv.tv_workspace_size(2, 5, 100))
+    args.update(kw)
+    return tv.tv_verify_stats(**args)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(batch=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=0.0), tv.TV_ERR_INVALID_ARG),
+    (dict(parents=None), tv.TV_ERR_INVALID_ARG),
+    (dict(target_max=None), tv.TV_ERR_INVALID_ARG),
+    (dict(target_sum=None), tv.TV_ERR_INVALID_ARG),
+    (dict(draft_max=None), tv.TV_ERR_INVALID_ARG),
+    (dict(draft_sum=None), tv.TV_ERR_INVALID_ARG),
+    (dict(target_sum=A + 4), tv.TV_ERR_INVALID_ARG),
+    (dict(draft_max=A + 2), tv.TV_ERR_INVALID_ARG),
+    (dict(workspace=None), tv.TV_ERR_WORKSPACE),
+    (dict(num_nodes=tv.TV_MAX_NODES + 1), tv.TV_ERR_UNSUPPORTED),
+])
+def test_verify_stats_argument_errors_launch_nothing(kw, want):
+    assert call_stats(**kw) == want
+
+
+def test_verify_stats_empty_batch_is_ok():
+    assert call_stats(batch=0, parents=None, tokens=None, target_logits=None, draft_logits=None,
+                      uniforms=None, target_max=None, target_sum=None, draft_max=None,
+                      draft_sum=None, accept_len=None, accepted_node=None, bonus_token=None,
+                      status=None, workspace=None, workspace_bytes=0) == tv.TV_OK
+
+
+def call_lmhead(**kw):
+    args = dict(rows=4, hidden_size=64, vocab=1000, hidden=A, weight=A + 0x1000,
+                temperature=1.0, logits=A, row_max=A, row_sum=A, workspace=WS,
+                workspace_bytes=tv.tv_lmhead_workspace_size(4, 1000))
+    args.update(kw)
+    return tv.tv_lmhead_stats(**args)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(rows=-1), tv.TV_ERR_INVALID_ARG),
+    (dict(hidden_size=4), tv.TV_ERR_INVALID_ARG),
+    (dict(hidden_size=60), tv.TV_ERR_UNSUPPORTED),
+    (dict(vocab=1), tv.TV_ERR_INVALID_ARG),
+    (dict(vocab=tv.TV_MAX_VOCAB + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(rows=tv.TV_MAX_LMHEAD_ROWS + 1), tv.TV_ERR_UNSUPPORTED),
+    (dict(hidden_size=tv.TV_MAX_HIDDEN + 8), tv.TV_ERR_UNSUPPORTED),
+    (dict(temperature=float("nan")), tv.TV_ERR_INVALID_ARG),
+    (dict(temperature=1e-5), tv.TV_ERR_UNSUPPORTED),
+    (dict(hidden=None), tv.TV_ERR_INVALID_ARG),
+    (dict(weight=None), tv.TV_ERR_INVALID_ARG),
+    (dict(logits=None), tv.TV_ERR_INVALID_ARG),
+    (dict(row_max=None), tv.TV_ERR_INVALID_ARG),
+    (dict(row_sum=None), tv.TV_ERR_INVALID_ARG),
+    (dict(hidden=A + 8), tv.TV_ERR_INVALID_ARG),
+    (dict(weight=A + 0x1008), tv.TV_ERR_INVALID_ARG),
+    (dict(logits=A + 1), tv.TV_ERR_INVALID_ARG),
+    (dict(row_sum=A + 4), tv.TV_ERR_INVALID_ARG),
+    (dict(workspace=None), tv.TV_ERR_WORKSPACE),
+    (dict(workspace=WS + 64), tv.TV_ERR_WORKSPACE),
+    (dict(workspace_bytes=16), tv.TV_ERR_WORKSPACE),
+])
+def test_lmhead_argument_errors_launch_nothing(kw, want):
+    assert call_lmhead(**kw) == want
+
+
+def test_lmhead_empty_and_workspace_size():
+    assert call_lmhead(rows=0, hidden=None, weight=None, logits=None, row_max=None,
+                       row_sum=None, workspace=None, workspace_bytes=0) == tv.TV_OK
+    assert tv.tv_lmhead_workspace_size(0, 1000) == 0
+    assert tv.tv_lmhead_workspace_size(1, 1) == 0
+    a = tv.tv_lmhead_workspace_size(16640, 128256)
+    assert a % 256 == 0 and a >= 2 * 16640 * 1002 * 4

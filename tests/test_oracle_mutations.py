@@ -259,3 +259,35 @@ def test_sampler_mutation_is_caught(monkeypatch, fn):
     not repeat, and an ignored temperature."""
     monkeypatch.setattr(_DS, "draw_tree_tokens", fn)
     assert P.first_failure([P.pin_draft_sampler_law, P.pin_draft_sampler_statuses]) is not None
+
+
+import oracle.lmhead as _LM  # noqa: E402
+
+_lm_logits_orig = _LM.logits
+_lm_stats_orig = _LM.row_stats
+
+
+def _lm_logits_dropped_last_k(hidden, weight):
+    x = O.to_f64(hidden)[:, :-1]
+    w = O.to_f64(weight)[:, :-1]
+    return x @ w.T
+
+
+def _lm_stats_no_temperature(z, T):
+    return _lm_stats_orig(z, 1.0)
+
+
+def _lm_stats_unshifted(z, T):
+    z = O.to_f64(z)
+    T = float(np.float32(T))
+    return z.max(axis=-1), np.exp(z / T).sum(axis=-1)
+
+
+@pytest.mark.parametrize("attr,fn", [("logits", _lm_logits_dropped_last_k),
+                                     ("row_stats", _lm_stats_no_temperature),
+                                     ("row_stats", _lm_stats_unshifted)])
+def test_lmhead_mutation_is_caught(monkeypatch, attr, fn):
+    """The LM-head pins catch a dropped hidden column, an ignored temperature
+    and a sum taken without the maximum subtracted."""
+    monkeypatch.setattr(_LM, attr, fn)
+    assert P.first_failure([P.pin_lmhead_logits, P.pin_row_stats]) is not None
