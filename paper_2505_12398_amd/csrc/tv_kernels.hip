@@ -2252,11 +2252,10 @@ struct SampleParams {
   int batch, num_nodes, vocab, mode;
 };
 
-constexpr int kSampleChunk = 64;        // units per chunk: one per lane of a wave
-// chunks of a row: at most 2^17 vectors plus 14 head and tail elements
-// (V <= 2^20 bf16 or 2^19 fp32), so 2049
+// chunk sums held per row: chunks of 8 units up to 16384 units (about 2^17
+// bf16 tokens), larger chunks (at most 64 units) up to the vocabulary limits
+// (2^17 vectors plus 14 head and tail elements)
 constexpr int kSampleMaxChunks = 2056;
-constexpr int kRowChunksInFlight = 8;      // chunks a wave loads before it sums them
 
 struct SampleSmem {
   double cs[kSampleMaxChunks];     // chunk weight sums, in the row's frame once rescaled
@@ -2412,89 +2411,94 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   const T* row = static_cast<const T*>(S.draft) + (static_cast<size_t>(b) * n1 + j) *
                                                       static_cast<size_t>(S.vocab);
   const RowWeights<T, A> rw{row, row_geom(row, S.vocab), ar, &sm};
+  constexpr int E = RowWeights<T, A>::E;
   const int U = rw.units();
-  const int C = (U + kSampleChunk - 1) / kSampleChunk;
-  if (C > kSampleMaxChunks) {      // beyond the vocabulary limits the host checks
+  // chunks of cu consecutive units, cu a multiple of 8, at most
+  // kSampleMaxChunks of them (cu = 8 up to about 2^17 bf16 tokens)
+  const int cu = 8 * max(1, (U + 8 * kSampleMaxChunks - 1) / (8 * kSampleMaxChunks));
+  const int C = (U + cu - 1) / cu;
+  if (C > kSampleMaxChunks || cu > 64) {   // beyond the vocabulary limits the host checks
     if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_DEGENERATE));
     return;
   }
 
-  // One read of the row: wave w sums chunks w, w + 4, ..., with
-  // kRowChunksInFlight chunks' loads issued together; the chunks of one such
-  // round share the frame of their maximum. Chunk sums are fp32 on the fast
-  // path and fp64 on the precise one. The fp32 butterfly over a chunk's 64
-  // unit sums has a relative error of at most about 6 * 2^-24 of the chunk's
-  // sum, hence of the row's total W whatever share of the row the chunk
-  // holds; that is below the 1e-6 * W near-tie band, so it can move a draw
-  // only at a near-tie.
-  float wmax = -INFINITY;
-  for (int c0 = wave; c0 < C; c0 += kNW * kRowChunksInFlight) {
-    float x[kRowChunksInFlight][RowWeights<T, A>::E];
-    int uu[kRowChunksInFlight];
+  // One read of the row. Thread t sums chunks t, t + 256, ... on its own, 8
+  // units at a time (8 16-byte vectors, or head and tail elements at the two
+  // ends of the row), the next 8 units' loads in flight while the current ones
+  // are summed; a chunk keeps the frame of its running maximum (Online). No
+  // reduction across threads until the row is read. A chunk's sum is the
+  // fp64 sum of fp32 sums of 8 units on the fast path (fp64 terms on the
+  // precise one): relative error about 64 * 2^-24 of the chunk's sum, hence
+  // of the row's total W, below the 1e-6 * W near-tie band.
+  const int nsb = cu / 8;                        // 8-unit blocks per chunk
+  const int my_chunks = C > tid ? (C - tid + kNT - 1) / kNT : 0;
+  const int items = my_chunks * nsb;
+  auto block_unit = [&](int i) { return (tid + kNT * (i / nsb)) * cu + 8 * (i % nsb); };
+  auto pure = [&](int ub) { return ub >= rw.g.head && ub + 8 <= rw.g.head + rw.g.nvec; };
+  auto load_block = [&](int ub, uint4 (&v)[8]) {
+    if (pure(ub)) {
 #pragma unroll
-    for (int i = 0; i < kRowChunksInFlight; ++i) {
-      const int c = c0 + i * kNW;
-      const int u = c * kSampleChunk + lane;
-      uu[i] = u < U ? u : U - 1;                  // clamped: the load is always in the row
+      for (int e = 0; e < 8; ++e) v[e] = load16(row, rw.g.head, ub - rw.g.head + e);
     }
-    if (rw.g.nvec > 0) {
-      // every lane loads a 16-byte vector of the row (index clamped into the
-      // vectors) before anything is used, so all the round's loads are in
-      // flight together; lanes whose unit is a head or tail element then
-      // replace it with that element
-      uint4 raw[kRowChunksInFlight];
+  };
+  float tmax = -INFINITY;
+  Online o = online_init(ar);
+  uint4 cur[8], nxt[8];
+  if (items > 0) load_block(block_unit(0), cur);
+  for (int i = 0; i < items; ++i) {
+    if (i + 1 < items) load_block(block_unit(i + 1), nxt);
+    const int ub = block_unit(i);
+    if (i % nsb == 0) o = online_init(ar);
+    float x[8][E];
+    if (pure(ub)) {
 #pragma unroll
-      for (int i = 0; i < kRowChunksInFlight; ++i) {
-        const int v = min(max(uu[i] - rw.g.head, 0), rw.g.nvec - 1);
-        raw[i] = load16(row, rw.g.head, v);
-      }
-#pragma unroll
-      for (int i = 0; i < kRowChunksInFlight; ++i) pin(raw[i]);
-#pragma unroll
-      for (int i = 0; i < kRowChunksInFlight; ++i) {
-        Elem<T>::unpack(raw[i], x[i]);
-        if (rw.count(uu[i]) != RowWeights<T, A>::E) rw.load(uu[i], x[i]);
+      for (int e = 0; e < 8; ++e) {
+        pin(cur[e]);
+        Elem<T>::unpack(cur[e], x[e]);
       }
     } else {
+      for (int e = 0; e < 8; ++e) {
+        if (ub + e < U) {
+          rw.load(ub + e, x[e]);
+        } else {
 #pragma unroll
-      for (int i = 0; i < kRowChunksInFlight; ++i) rw.load(uu[i], x[i]);
-    }
-    float lm = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < kRowChunksInFlight; ++i) {
-      const int c = c0 + i * kNW;
-      if (c < C && c * kSampleChunk + lane < U) lm = fmaxf(lm, rw.vmax(x[i]));
-    }
-    const float M = wave_max(lm);
-    const double fr = (M > -INFINITY) ? ar.frame(M) : 0.0;   // all -inf: weights 0 (or NaN)
-#pragma unroll
-    for (int i = 0; i < kRowChunksInFlight; ++i) {
-      const int c = c0 + i * kNW;
-      if (c >= C) break;
-      const bool in = c * kSampleChunk + lane < U;
-      const double us = in ? rw.sum_of(uu[i], x[i], fr) : 0.0;
-      double sum;
-      if constexpr (A::kPrecise) {
-        sum = wave_sum(us);
-      } else {
-        float v = static_cast<float>(us);
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-        sum = static_cast<double>(v);
-      }
-      if (lane == 0) {
-        sm.cs[c] = sum;
-        sm.cm[c] = M;
+          for (int q = 0; q < E; ++q) x[e][q] = -INFINITY;
+        }
       }
     }
-    wmax = fmaxf(wmax, M);
+    float vmax = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int q = 0; q < E; ++q) vmax = fmaxf(vmax, x[e][q]);
+    online_raise(o, vmax, ar);
+    if constexpr (A::kPrecise) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int q = 0; q < E; ++q) o.s += ar.ex(x[e][q], o.c);
+    } else {
+      const float cf32 = static_cast<float>(o.c);
+      float part = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int q = 0; q < E; ++q) part += fast_exp2(fmaf(x[e][q], ar.k, cf32));
+      o.s += static_cast<double>(part);
+    }
+    if (i % nsb == nsb - 1) {
+      const int c = tid + kNT * (i / nsb);
+      // the sum in the frame of the chunk's maximum (that of the sentinel, with
+      // sum 0 or NaN, when the chunk has no finite value)
+      sm.cs[c] = o.s;
+      sm.cm[c] = o.m;
+      tmax = fmaxf(tmax, o.m);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cur[e] = nxt[e];
   }
-  if (lane == 0) ws.red_f[wave] = wmax;
-  __syncthreads();
-  float rowmax = ws.red_f[0];
-#pragma unroll
-  for (int w = 1; w < kNW; ++w) rowmax = fmaxf(rowmax, ws.red_f[w]);
-  __syncthreads();
+  float rowmax = tmax, unused_max = -INFINITY;
+  block_max2(ws, rowmax, unused_max);
   if (!(rowmax > -INFINITY) || rowmax == INFINITY) {
     if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_NONFINITE));
     return;
@@ -2559,8 +2563,9 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
       const int c = sm.chunk;
       int tok = -1;
       if (c >= 0) {
-        const int u = c * kSampleChunk + lane;
-        const double us = u < U ? rw.unit_sum(u, cf) : 0.0;
+        const int u = c * cu + lane;
+        const bool mine = lane < cu && u < U;
+        const double us = mine ? rw.unit_sum(u, cf) : 0.0;
         double inc = us;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
@@ -2569,7 +2574,7 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
         }
         const double run = sm.run;
         const uint64_t pos = __ballot(us > 0.0);
-        const uint64_t hitm = __ballot(u < U && us > 0.0 && run + inc > target);
+        const uint64_t hitm = __ballot(mine && us > 0.0 && run + inc > target);
         const int L = hitm ? __ffsll(static_cast<unsigned long long>(hitm)) - 1
                            : (pos ? 63 - __clzll(static_cast<long long>(pos)) : -1);
         int t = -1, lp = -1;
@@ -2594,19 +2599,18 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
                     : (tok < rw.g.head + rw.g.nvec * RowWeights<T, A>::E
                            ? rw.g.head + (tok - rw.g.head) / RowWeights<T, A>::E
                            : rw.g.head + rw.g.nvec + (tok - rw.g.head - rw.g.nvec * RowWeights<T, A>::E));
-      const int c = u / kSampleChunk;
-      if (tid == 0) {
-        float x[RowWeights<T, A>::E];
-        rw.load(u, x);
-        const int e = tok - rw.first(u);
-        float z = x[0];
-#pragma unroll
-        for (int i = 1; i < RowWeights<T, A>::E; ++i)
-          if (i == e) z = x[i];
-        const double w = static_cast<double>(rw.weight(tok, z, cf));
-        const double v = sm.cs[c] - w;
-        sm.cs[c] = v > 0.0 ? v : 0.0;
-        sm.removed[sm.nremoved++] = tok;
+      const int c = u / cu;
+      if (tid == 0) sm.removed[sm.nremoved++] = tok;
+      __syncthreads();
+      // The chunk's sum is formed again from its units, the drawn token now
+      // weighing 0. Subtracting the token's weight instead would cancel: when
+      // it held most of the row's mass, the rounding of the old sum (relative
+      // to the old total) would be large against the new total.
+      if (tid < 64) {
+        const int uu = c * cu + lane;
+        const double us = (lane < cu && uu < U) ? rw.unit_sum(uu, cf) : 0.0;
+        const double v = wave_sum(us);
+        if (lane == 0) sm.cs[c] = v;
       }
       __syncthreads();
       if (c >= cb && c < ce) {

@@ -156,3 +156,28 @@ def test_drawn_trees_verify(mode):
     rep = parity.check(bt, False, label=f"drawn-verify mode={mode}")
     print(f"drawn trees mode={mode}: {rep.summary()}", flush=True)
     assert not rep.failures, "\n".join(rep.failures[:5])
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_peaked_rows(mode):
+    """Rows where one token holds most of the mass (its logit raised by 12
+    above the row's N(0, 3^2) values, so it holds more than half of the
+    tempered draft at T = 1), V = 128256 bf16: the fast path's chunk sums
+    are fp32 sums of unit sums whatever share of the row a chunk has; draws
+    must still match the oracle (near-ties aside). 24 random 9-node trees."""
+    rng = np.random.default_rng(23)
+    B, n1, V = 24, 9, 128256
+    par = np.zeros((B, n1), np.int32)
+    par[:, 0] = -1
+    for b in range(B):
+        for i in range(1, n1):
+            par[b, i] = rng.integers(max(0, i - 3), i)
+    z = rng.normal(0.0, 3.0, (B, n1, V)).astype(np.float32)
+    hot = rng.integers(0, V, (B, n1))
+    for b in range(B):
+        for i in range(n1):
+            z[b, i, hot[b, i]] = z[b, i].max() + 12.0
+    draft = torch.as_tensor(z, device=DEV).to(torch.bfloat16)
+    u = torch.as_tensor(W.uniforms_np(rng, (B, n1)), device=DEV)
+    check_sampler(torch.as_tensor(par, device=DEV), draft, 1.0, u, mode,
+                  label=f"peaked mode={mode}")
