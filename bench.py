@@ -105,25 +105,46 @@ def algorithmic_bytes(counters, vocab, elem_bytes, num_nodes, status=None):
 TV_NUM_COUNTERS = 4
 
 
+_CPU_TREES = None
+
+
+def _one_thread():
+    """Pool initialiser: one BLAS/OpenMP thread per worker process, so that
+    `workers` processes use `workers` cores."""
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(1)
+
+
+def _oracle_idx(b):
+    """The oracle on tree b of the trees the parent process holds (inherited
+    by fork, never sent); returns the result without its V-vector."""
+    trees, T, mode = _CPU_TREES
+    r = _oracle_one((trees[b], T, mode))
+    r.y_weights = None
+    return r
+
+
 def cpu_baseline(batch, gpu_outs: dict, sample: int, workers: int):
     """The oracle on the first `sample` trees of one step, on host cores, with
-    parity of those trees against each of the GPU outputs (by label)."""
+    parity of those trees against each of the GPU outputs (by label). The
+    trees are copied to host memory before the clock starts and the workers
+    inherit them, so the time is the oracle's own."""
+    global _CPU_TREES
     import multiprocessing as mp
-
-    import numpy as np
 
     import workloads as W
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     import parity  # noqa: E402  (test infrastructure: oracle comparison)
 
-    trees = [W.tree_numpy(batch, b) for b in range(sample)]
-    T = batch["temperature"]
-    mode = batch["mode"]
-    args = [(t, T, mode) for t in trees]
-    t0 = time.perf_counter()
-    with mp.get_context("fork").Pool(workers) as pool:
-        refs = pool.map(_oracle_one, args)
-    dt = time.perf_counter() - t0
+    _CPU_TREES = ([W.tree_numpy(batch, b) for b in range(sample)], batch["temperature"],
+                  batch["mode"])
+    try:
+        t0 = time.perf_counter()
+        with mp.get_context("fork").Pool(workers, initializer=_one_thread) as pool:
+            refs = pool.map(_oracle_idx, range(sample), chunksize=1)
+        dt = time.perf_counter() - t0
+    finally:
+        _CPU_TREES = None
     reps = {}
     for label, gpu_out in gpu_outs.items():
         g = parity.host_outputs(gpu_out)
@@ -734,16 +755,20 @@ def main():
                                        sample, workers)
         # one process, one core: the oracle on the first trees, in this process
         n_single = min(8, B)
-        t0 = time.perf_counter()
-        for b in range(n_single):
-            _oracle_one((W.tree_numpy(batch, b), batch["temperature"], mode))
-        per_core = n_single / (time.perf_counter() - t0)
+        single = [W.tree_numpy(batch, b) for b in range(n_single)]
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            for t in single:
+                _oracle_one((t, batch["temperature"], mode))
+            per_core = n_single / (time.perf_counter() - t0)
         res["cpu_baseline"] = {
             "value": tps, "unit": "trees/s", "cores": workers, "kind": "oracle",
             "sample": f"first {sample} trees of timed step {args.steps - 1} "
                       f"({secs:.1f} s wall, float64 numpy, one process per core)",
             "per_core": {"value": per_core, "unit": "trees/s",
-                         "sample": f"first {n_single} trees of the same step, one process"},
+                         "sample": f"first {n_single} trees of the same step, one process, "
+                                   "one BLAS thread"},
             "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
         }
         rep, rth = reps["timed"], reps["theta"]

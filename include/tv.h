@@ -127,7 +127,8 @@ enum {
 #define TV_MIN_TEMPERATURE 1.0e-3f
 #define TV_MAX_TEMPERATURE 1.0e3f
 #define TV_NUM_COUNTERS 4
-#define TV_MAX_LMHEAD_ROWS (1 << 24)    /* rows of one tv_lmhead_stats call */
+#define TV_MAX_LMHEAD_ROWS (1 << 18)    /* rows of one tv_lmhead_stats call (its grid of
+                                           128 x 128 tiles then stays below 2^24 workgroups) */
 #define TV_MAX_HIDDEN (1 << 16)         /* hidden size of tv_lmhead_stats */
 
 /*

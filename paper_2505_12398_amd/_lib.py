@@ -19,7 +19,7 @@ TV_MAX_NODES = 1024
 TV_MAX_VOCAB = 1 << 20
 TV_MAX_VOCAB_F32 = 1 << 19
 TV_NUM_COUNTERS = 4
-TV_MAX_LMHEAD_ROWS = 1 << 24
+TV_MAX_LMHEAD_ROWS = 1 << 18
 TV_MAX_HIDDEN = 1 << 16
 
 

@@ -13,9 +13,9 @@
 // multiplied from LDS. Both operands are K-contiguous (hidden [M][K], weight
 // [N][K]), so every MFMA operand fragment is one 16-byte LDS read; LDS rows
 // are padded by 16 bytes against bank conflicts. Each XCD gets a contiguous
-// run of tiles in which row tiles of one column tile follow each other, so a
-// slice of the weight is read from HBM about once per XCD and reused from its
-// L2 by the row tiles.
+// run of tiles, ordered in bands of 8 row tiles column tile by column tile,
+// so the 8 x 8 or so tiles it runs at once read each slice of the hidden
+// states and of the weight once from HBM and share it through the XCD's L2.
 //
 // Epilogue. Each accumulator is rounded to bf16 (round to nearest even) and
 // stored. Per row, the wavefront reduces its 64 columns (max, then the sum of
@@ -36,6 +36,7 @@ namespace {
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 constexpr int kLds = kBK + 8;          // padded LDS row, bf16 elements (144 bytes)
 constexpr int kThreads = 256;
+constexpr int kGroupM = 8;            // row tiles per band of the tile order
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
@@ -102,15 +103,19 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   // Workgroups are dealt to the 8 XCDs in turn (workgroup i to XCD i % 8):
-  // the logical tile order gives each XCD a contiguous run of tiles, and
-  // consecutive tiles share a column tile of the weight, so a weight slice is
-  // reused from that XCD's L2 by the row tiles.
-  const unsigned nb = gridDim.x;
-  unsigned lb = blockIdx.x;
-  if (nb % 8u == 0) lb = (lb % 8u) * (nb / 8u) + lb / 8u;
+  // the remap gives each XCD a contiguous run of logical tiles (any grid
+  // size), and the logical order walks bands of kGroupM row tiles column tile
+  // by column tile, so the tiles an XCD runs at once form a block of about
+  // kGroupM x kGroupM that shares each operand slice through its L2.
+  const unsigned nb = gridDim.x, per = nb / 8u, rem = nb % 8u;
+  const unsigned xcd = blockIdx.x % 8u, idx = blockIdx.x / 8u;
+  const unsigned lb = xcd < rem ? xcd * (per + 1u) + idx : rem * (per + 1u) + (xcd - rem) * per + idx;
   const int tiles_m = (P.M + kBM - 1) / kBM;
-  const int tm = static_cast<int>(lb) % tiles_m;
-  const int tn = static_cast<int>(lb) / tiles_m;
+  const int band = static_cast<int>(lb) / (kGroupM * P.tiles_n);
+  const int in_band = static_cast<int>(lb) - band * kGroupM * P.tiles_n;
+  const int gm = min(kGroupM, tiles_m - band * kGroupM);
+  const int tm = band * kGroupM + in_band % gm;
+  const int tn = in_band / gm;
   const int m0 = tm * kBM, n0 = tn * kBN;
 
   f32x16 acc[2][2];
