@@ -255,8 +255,8 @@ int tv_verify_stats(int32_t batch, int32_t num_nodes, int32_t vocab,
  * the same kernel from the rounded logits it holds, so they cost no pass over
  * the logits. A NaN or infinite logit makes its row's sum NaN or infinite.
  * workspace: device buffer of tv_lmhead_workspace_size(rows, vocab) bytes,
- * 256-byte aligned (per-tile partial statistics). Returns a tv_status_t;
- * argument errors launch nothing.
+ * 256-byte aligned (a maximum and a sum per row and 256-column tile).
+ * Returns a tv_status_t; argument errors launch nothing.
  */
 size_t tv_lmhead_workspace_size(int32_t rows, int32_t vocab);
 int tv_lmhead_stats(int32_t rows, int32_t hidden_size, int32_t vocab, const void* hidden,

@@ -102,7 +102,7 @@ struct LmheadArgs {
   double* row_sum;        // [M]
 };
 
-constexpr int kLmheadTileN = 128;   // logits columns per workgroup
+constexpr int kLmheadTileN = 256;   // logits columns per workgroup
 
 // Workspace of tv_lmhead_stats: one (max, sum) partial per row and column tile.
 struct LmheadLayout {

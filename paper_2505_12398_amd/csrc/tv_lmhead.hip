@@ -5,25 +5,27 @@
 // logits is needed to compute them (the distributions M_b and M_s of the
 // problem statement, Alg. 3 REQUIRE, are softmax(logits / T) per row).
 //
-// Tiling. A workgroup of 256 threads (4 wavefronts, 2 x 2) computes a 128 x 128
-// tile of logits; each wavefront a 64 x 64 sub-tile as 2 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16 (fp32 accumulation). K advances 64 at a time: the
-// next K-slice of both operand tiles is loaded from global memory into
-// registers (16-byte loads, coalesced along K) while the current one is
-// multiplied from LDS. Both operands are K-contiguous (hidden [M][K], weight
-// [N][K]), so every MFMA operand fragment is one 16-byte LDS read; LDS rows
-// are padded by 16 bytes against bank conflicts. Each XCD gets a contiguous
-// run of tiles, ordered in bands of 8 row tiles column tile by column tile,
-// so the 8 x 8 or so tiles it runs at once read each slice of the hidden
-// states and of the weight once from HBM and share it through the XCD's L2.
+// Tiling. A workgroup of 256 threads (4 wavefronts, 2 x 2) computes a 256 x 256
+// tile of logits; each wavefront a 128 x 128 sub-tile as 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16 (fp32 accumulation, 256 accumulator registers per
+// lane, one wavefront per SIMD). K advances 64 at a time through two LDS
+// buffers: while the products of one K-slice are formed from one buffer, the
+// next slice of both operand tiles is loaded from global memory into
+// registers (16-byte loads, coalesced along K) and then stored into the other
+// buffer, so one barrier per K-slice suffices. Both operands are K-contiguous
+// (hidden [M][K], weight [N][K]), so every MFMA operand fragment is one
+// 16-byte LDS read; LDS rows are padded by 16 bytes against bank conflicts.
+// Each XCD gets a contiguous run of tiles, ordered in bands of 8 row tiles
+// column tile by column tile, so the tiles it runs at once read each slice of
+// the hidden states and of the weight once from HBM and share it through the
+// XCD's L2.
 //
-// Epilogue. Each accumulator is rounded to bf16 (round to nearest even) and
-// stored. Per row, the wavefront reduces its 64 columns (max, then the sum of
-// 2^((z - max) k), k = log2(e)/T, in fp32) across the 32 lanes that hold the
-// row; the two wavefronts sharing a row merge through LDS; the workgroup
-// writes one (max, sum) partial per row and column tile. A second kernel
-// merges a row's partials in fp64 (exact power-of-two rescaling of each
-// partial to the row maximum).
+// Epilogue. Each accumulator is rounded to bf16 (round to nearest even) into
+// the tile in LDS; the tile is stored in 16-byte vectors along its rows; then
+// each thread reads one row of it back and forms the row's maximum and its sum
+// of 2^((z - max) k), k = log2(e)/T, in fp32: one (max, sum) partial per row
+// and column tile. A second kernel merges a row's partials in fp64 (exact
+// power-of-two rescaling of each partial to the row maximum).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -33,10 +35,16 @@
 
 namespace {
 
-constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kBM = 256, kBN = tv::kLmheadTileN, kBK = 64;
 constexpr int kLds = kBK + 8;          // padded LDS row, bf16 elements (144 bytes)
 constexpr int kThreads = 256;
-constexpr int kGroupM = 8;            // row tiles per band of the tile order
+constexpr int kGroupM = 8;             // row tiles per band of the tile order
+constexpr int kVecs = kBM * kBK / 8 / kThreads;   // 16-byte vectors per thread and operand
+#ifndef TV_LMHEAD_STAGING
+#define TV_LMHEAD_STAGING 2
+#endif
+constexpr int kStaging = TV_LMHEAD_STAGING;        // register sets of operand slices in flight
+static_assert(kBM == kBN, "one load pattern serves both operands");
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
@@ -56,57 +64,107 @@ struct LmParams {
 // fp32 -> bf16 bits, round to nearest even (NaN kept quiet)
 __device__ __forceinline__ uint16_t to_bf16(float f) {
   const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t quiet = (u >> 16) | 0x40u;
+  return static_cast<uint16_t>((u & 0x7fffffffu) > 0x7f800000u ? quiet : rounded);
 }
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// One K-slice of a 128-row operand tile: 1024 16-byte vectors, four per
+// One K-slice of a 256-row operand tile: 2048 16-byte vectors, eight per
 // thread (vector v = thread + 256 q: row v / 8, 8 bf16 at column 8 (v % 8)).
-// Rows or columns outside the matrix read as zeros.
+// The loads are buffer loads over the tile's rows: the hardware returns zeros
+// for a vector beyond the last row of the matrix, and a vector beyond the
+// last column is given an offset past the range (at most 256 rows of 2^16
+// bf16, 32 MiB), so no load branches.
+constexpr int kBufferConfig = 0x00020000;   // buffer descriptor word 3 on gfx9-family GPUs
+
 struct Slice {
-  uint4 v[4];
-  __device__ __forceinline__ void load(const uint16_t* base, int rows, int row0, int K, int k0) {
+  uint4 v[kVecs];
+  __device__ __forceinline__ static __amdgpu_buffer_rsrc_t tile(const uint16_t* base, int rows,
+                                                                int row0, int K) {
+    const int nrows = min(kBM, rows - row0);
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(base + static_cast<size_t>(row0) * K), 0,
+        nrows * K * static_cast<int>(sizeof(uint16_t)), kBufferConfig);
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int K, int k0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kVecs; ++q) {
       const int idx = threadIdx.x + kThreads * q;
-      const int r = row0 + (idx >> 3);
       const int c = k0 + 8 * (idx & 7);
-      if (r < rows && c < K) {
-        v[q] = *reinterpret_cast<const uint4*>(base + static_cast<size_t>(r) * K + c);
-      } else {
-        v[q] = make_uint4(0, 0, 0, 0);
-      }
+      const int past = (K - 1 - c) >> 31;      // -1 beyond the last column, else 0
+      const int off = (((idx >> 3) * K + c) * static_cast<int>(sizeof(uint16_t))) |
+                      (past & 0x7fffffff);      // at least 2^31 - 1 > range: reads zeros
+      v[q] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
     }
   }
   __device__ __forceinline__ void store(uint16_t* lds) const {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kVecs; ++q) {
       const int idx = threadIdx.x + kThreads * q;
       *reinterpret_cast<uint4*>(lds + (idx >> 3) * kLds + 8 * (idx & 7)) = v[q];
     }
   }
 };
 
-__device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int row, int k) {
-  const uint4 u = *reinterpret_cast<const uint4*>(lds + row * kLds + k);
+__device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int off) {
+  const uint4 u = *reinterpret_cast<const uint4*>(lds + off);
   return __builtin_bit_cast(bf16x8, u);
 }
 
+constexpr int kOperandLds = kBM * kLds;       // bf16 elements of one operand buffer
+constexpr int kTilePitch = kBN + 8;           // bf16 elements per row of the rounded tile in LDS
+static_assert(kBM * kTilePitch <= 4 * kOperandLds, "the rounded tile fits the operand buffers");
+
+// Statistics of one row of the rounded tile in LDS over its first `cols`
+// columns (kCols > 0: all kCols, with no masking): the maximum, then the sum
+// of 2^((z - max) k) in fp32. The hardware exp2 gives 0 for -inf, so a row
+// whose columns are all -inf sums 0; NaN or +inf propagate into the sum (NaN
+// is not ordered by fmaxf and surfaces there).
+template <int kCols>
+__device__ __forceinline__ void row_stats(const uint16_t* tr, int cols, float k, float& m_out,
+                                          float& s_out) {
+  float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll 8
+  for (int j = 0; j < kBN / 8; ++j) {
+    const uint4 q = *reinterpret_cast<const uint4*>(tr + 8 * j);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
+      if (kCols > 0 || 8 * j + e < cols) mx[e & 3] = fmaxf(mx[e & 3], z);
+    }
+  }
+  const float m = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
+  const float c = (m > -INFINITY) ? -m * k : 0.0f;
+  float sm[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 8
+  for (int j = 0; j < kBN / 8; ++j) {
+    const uint4 q = *reinterpret_cast<const uint4*>(tr + 8 * j);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
+      if (kCols > 0 || 8 * j + e < cols) sm[e & 3] += __builtin_amdgcn_exp2f(fmaf(z, k, c));
+    }
+  }
+  m_out = m;
+  s_out = (sm[0] + sm[1]) + (sm[2] + sm[3]);
+}
+
 __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[kBM * kLds];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[kBN * kLds];
-  __shared__ float red_m[2][kBM];
-  __shared__ float red_s[2][kBM];
+  // two buffers of both operands; after the products, the first holds the
+  // row reductions of the epilogue
+  __shared__ __attribute__((aligned(16))) uint16_t lds[4 * kOperandLds];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   // Workgroups are dealt to the 8 XCDs in turn (workgroup i to XCD i % 8):
   // the remap gives each XCD a contiguous run of logical tiles (any grid
   // size), and the logical order walks bands of kGroupM row tiles column tile
-  // by column tile, so the tiles an XCD runs at once form a block of about
-  // kGroupM x kGroupM that shares each operand slice through its L2.
+  // by column tile, so the tiles an XCD runs at once share each operand slice
+  // through its L2.
   const unsigned nb = gridDim.x, per = nb / 8u, rem = nb % 8u;
   const unsigned xcd = blockIdx.x % 8u, idx = blockIdx.x / 8u;
   const unsigned lb = xcd < rem ? xcd * (per + 1u) + idx : rem * (per + 1u) + (xcd - rem) * per + idx;
@@ -118,121 +176,168 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   const int tn = in_band / gm;
   const int m0 = tm * kBM, n0 = tn * kBN;
 
-  f32x16 acc[2][2];
+  f32x16 acc[4][4];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
 
-  Slice sa, sb;
-  sa.load(P.x, P.M, m0, P.K, 0);
-  sb.load(P.w, P.N, n0, P.K, 0);
+  const __amdgpu_buffer_rsrc_t ra = Slice::tile(P.x, P.M, m0, P.K);
+  const __amdgpu_buffer_rsrc_t rb = Slice::tile(P.w, P.N, n0, P.K);
   const int lr = lane & 31, lh = lane >> 5;
-  for (int k0 = 0; k0 < P.K; k0 += kBK) {
-    __syncthreads();                 // the previous slice has been consumed
-    sa.store(As);
-    sb.store(Bs);
-    __syncthreads();
-    if (k0 + kBK < P.K) {            // next slice in flight during the products
-      sa.load(P.x, P.M, m0, P.K, k0 + kBK);
-      sb.load(P.w, P.N, n0, P.K, k0 + kBK);
+  const int nk = (P.K + kBK - 1) / kBK;
+  const int fra = (wm * 128 + lr) * kLds + 8 * lh;      // this lane's fragment offsets
+  const int frb = (wn * 128 + lr) * kLds + 8 * lh;
+  // kStaging register sets of slices: with two, slice kt + 1 waits in one
+  // while slice kt + 2 is loaded into the other, so a load has two slices'
+  // products to arrive; with one, a load has one.
+  Slice sa[kStaging], sb[kStaging];
+  sa[0].load(ra, P.K, 0);
+  sb[0].load(rb, P.K, 0);
+  sa[0].store(lds);
+  sb[0].store(lds + kOperandLds);
+  if constexpr (kStaging == 2) {
+    sa[1].load(ra, P.K, kBK);
+    sb[1].load(rb, P.K, kBK);
+  }
+  __syncthreads();
+  // One K-slice: the products of slice kt from LDS buffer kt % 2 while slice
+  // kt + kStaging is loaded into a register set (beyond the last slice every
+  // vector is past the range and reads zeros) and slice kt + 1 is stored from
+  // its set into the other buffer, which was last read before the previous
+  // barrier (after the last slice it is stored into the buffer no one reads
+  // again).
+  auto slice = [&](const int kt, Slice& la, Slice& lb, const Slice& ka, const Slice& kb) {
+    // la/lb receive slice kt + kStaging; ka/kb hold slice kt + 1 (the same
+    // sets when kStaging is 1: loaded at the top, stored at the bottom)
+    const uint16_t* As = lds + (kt & 1) * 2 * kOperandLds;
+    const uint16_t* Bs = As + kOperandLds;
+    uint16_t* nxt = lds + ((kt + 1) & 1) * 2 * kOperandLds;
+    la.load(ra, P.K, (kt + kStaging) * kBK);
+    lb.load(rb, P.K, (kt + kStaging) * kBK);
+    // A fragments are reloaded for the next 16-deep step as soon as the four
+    // products that read them are issued; B fragments are double buffered
+    bf16x8 fa[4], fb[2][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) fa[a] = frag(As, fra + a * 32 * kLds);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) fb[0][b] = frag(Bs, frb + b * 32 * kLds);
+#pragma unroll
+    for (int s = 0; s < kBK / 16; ++s) {
+      const int cur = s & 1;
+      const bool next = s + 1 < kBK / 16;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[cur][b], acc[a][b],
+                                                              0, 0, 0);
+        if (next) {
+          fa[a] = frag(As, fra + a * 32 * kLds + 16 * (s + 1));
+          fb[cur ^ 1][a] = frag(Bs, frb + a * 32 * kLds + 16 * (s + 1));
+        }
+      }
+    }
+    ka.store(nxt);
+    kb.store(nxt + kOperandLds);
+    // instruction order of the slice: the first fragments; then per step
+    // four products, then two fragment reads for the next step, four times
+    // (the global loads spread over the first step's products); the stores
+    // of the next slice over the last step's products
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
 #pragma unroll
-    for (int kk = 0; kk < kBK; kk += 16) {
-      bf16x8 fa[2], fb[2];
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
 #pragma unroll
-      for (int a = 0; a < 2; ++a) fa[a] = frag(As, wm * 64 + a * 32 + lr, kk + 8 * lh);
-#pragma unroll
-      for (int b = 0; b < 2; ++b) fb[b] = frag(Bs, wn * 64 + b * 32 + lr, kk + 8 * lh);
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    }
+    __syncthreads();
+  };
+  if constexpr (kStaging == 1) {
+    for (int kt = 0; kt < nk; ++kt) slice(kt, sa[0], sb[0], sa[0], sb[0]);
+  } else {
+    // an odd count of slices gets one more, of zeros (every vector of it is
+    // past the range), which adds nothing to the products
+    for (int kt = 0; kt < nk; kt += 2) {
+      slice(kt, sa[0], sb[0], sa[1], sb[1]);
+      slice(kt + 1, sa[1], sb[1], sa[0], sb[0]);
     }
   }
 
-  // Epilogue: accumulator r of block (a, b) holds row
-  // m0 + 64 wm + 32 a + 8 (r / 4) + 4 lh + r % 4 and column n0 + 64 wn + 32 b + lr.
-  const float k = P.k32;
-  float zb[2][2][16];
+  // Epilogue. Accumulator r of block (a, b) holds row
+  // 128 wm + 32 a + 8 (r / 4) + 4 lh + r % 4 and column 128 wn + 32 b + lr of
+  // the tile. The rounded tile goes through LDS (the operand buffers are free
+  // now): stored from there in 16-byte vectors along rows, and read back one
+  // row per thread for the statistics, so no value crosses lanes.
+  uint16_t* tile = lds;                                   // [kBM][kTilePitch]
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int col = n0 + wn * 64 + b * 32 + lr;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        const uint16_t h = to_bf16(acc[a][b][r]);
-        if (row < P.M && col < P.N) P.logits[static_cast<size_t>(row) * P.N + col] = h;
-        zb[a][b][r] = col < P.N ? bf16_to_f32(h) : -INFINITY;
-      }
-    }
-  // row maxima over the wavefront's 64 columns: the two column blocks, then
-  // the 32 lanes of this half of the wavefront
-  float mx[2][16];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float v = fmaxf(zb[a][0][r], zb[a][1][r]);
-#pragma unroll
-      for (int off = 1; off < 32; off <<= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-      mx[a][r] = v;
-    }
-  // sums of 2^((z - max) k) in the frame of the wavefront's row maximum (a
-  // row whose maximum is -inf, every column masked or -inf, sums 0; NaN or
-  // +inf propagate)
-  float sm[2][16];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float m = mx[a][r];
-      const float c = (m > -INFINITY) ? -m * k : 0.0f;
-      float v = 0.0f;
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const float z = zb[a][b][r];
-        v += (z > -INFINITY) ? __builtin_amdgcn_exp2f(fmaf(z, k, c)) : (z != z ? z : 0.0f);
-      }
-#pragma unroll
-      for (int off = 1; off < 32; off <<= 1) v += __shfl_xor(v, off, 64);
-      sm[a][r] = v;
-    }
-  // the two wavefronts of a row band (wn = 0, 1) merge through LDS
-  if (lr == 0) {
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 4; ++b) {
+      const int col = wn * 128 + b * 32 + lr;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int rl = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        red_m[wn][rl] = mx[a][r];
-        red_s[wn][rl] = sm[a][r];
+        const int row = wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        tile[row * kTilePitch + col] = to_bf16(acc[a][b][r]);
       }
-  }
+    }
   __syncthreads();
-  if (tid < kBM) {
-    const int row = m0 + tid;
-    if (row < P.M) {
-      const float ma = red_m[0][tid], mb = red_m[1][tid];
-      const float sa_ = red_s[0][tid], sb_ = red_s[1][tid];
-      const float m = fmaxf(ma, mb);
-      float s;
-      if (!(m > -INFINITY)) {
-        s = sa_ + sb_;                                   // 0, or NaN
-      } else {
-        // frames -max * k as the terms used them (fp32 products)
-        const float cm = -m * k;
-        s = (ma > -INFINITY ? sa_ * __builtin_amdgcn_exp2f(cm - (-ma * k)) : sa_) +
-            (mb > -INFINITY ? sb_ * __builtin_amdgcn_exp2f(cm - (-mb * k)) : sb_);
+  // logits: thread t stores column vector t % 32 of rows t / 32, t / 32 + 8,
+  // ... (a row's 32 vectors by 32 consecutive threads), non-temporal: the
+  // logits are not read again by this kernel and should not displace the
+  // operand slices in the caches
+  const int cols = min(kBN, P.N - n0), rows = min(kBM, P.M - m0);
+  uint16_t* out = P.logits + static_cast<size_t>(m0) * P.N + n0;
+  if ((P.N & 7) == 0 && (reinterpret_cast<uintptr_t>(P.logits) & 15) == 0) {
+    typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+    const int c8 = 8 * (tid & 31);
+    if (c8 < cols) {                                      // cols is a multiple of 8 here
+      const uint16_t* src = tile + (tid >> 5) * kTilePitch + c8;
+      uint16_t* dst = out + static_cast<size_t>(tid >> 5) * P.N + c8;
+      const size_t step = static_cast<size_t>(8) * P.N;
+#pragma unroll 8
+      for (int row = tid >> 5; row < rows; row += 8) {
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(src),
+                                    reinterpret_cast<u32x4*>(dst));
+        src += 8 * kTilePitch;
+        dst += step;
       }
-      P.part_max[static_cast<size_t>(row) * P.tiles_n + tn] = m;
-      P.part_sum[static_cast<size_t>(row) * P.tiles_n + tn] = s;
     }
+  } else {
+    for (int e = tid; e < kBM * kBN; e += kThreads) {
+      const int row = e >> 8, c = e & 255;
+      if (row < rows && c < cols) out[static_cast<size_t>(row) * P.N + c] = tile[row * kTilePitch + c];
+    }
+  }
+  // statistics of row tid over the tile's columns
+  if (tid < rows) {
+    float m, sum;
+    if (cols == kBN) {
+      row_stats<kBN>(tile + tid * kTilePitch, kBN, P.k32, m, sum);
+    } else {
+      row_stats<0>(tile + tid * kTilePitch, cols, P.k32, m, sum);
+    }
+    const int row = m0 + tid;
+    P.part_max[static_cast<size_t>(row) * P.tiles_n + tn] = m;
+    P.part_sum[static_cast<size_t>(row) * P.tiles_n + tn] = sum;
   }
 }
 
