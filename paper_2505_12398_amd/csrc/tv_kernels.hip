@@ -2284,7 +2284,8 @@ __global__ void __launch_bounds__(256) sample_finish_kernel(SampleParams S) {
 
 // The weights of one row are 2^(z*k + c) in a frame c, grouped in units:
 // head elements (up to the first 16-byte boundary), 16-byte vectors, tail
-// elements, in token order; 64 consecutive units form a chunk. A unit's sum
+// elements, in token order; consecutive units form chunks (8 units each up to
+// about 2^17 bf16 tokens, more for larger rows). A unit's sum
 // and the running sum inside it are formed in the same order, so a rescan
 // reproduces the sum that chose it. Tokens already drawn (without
 // replacement) weigh 0.
