@@ -116,7 +116,7 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int off) {
 
 constexpr int kOperandLds = kBM * kLds;       // bf16 elements of one operand buffer
 constexpr int kTilePitch = kBN + 8;           // bf16 elements per row of the rounded tile in LDS
-static_assert(kBM * kTilePitch <= 4 * kOperandLds, "the rounded tile fits the operand buffers");
+static_assert((kBM / 2) * kTilePitch <= 2 * kOperandLds, "half the rounded tile fits a buffer");
 
 // Statistics of one row of the rounded tile in LDS over its first `cols`
 // columns (kCols > 0: all kCols, with no masking): the maximum, then the sum
@@ -155,9 +155,12 @@ __device__ __forceinline__ void row_stats(const uint16_t* tr, int cols, float k,
 }
 
 __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
-  // two buffers of both operands; after the products, the first holds the
-  // row reductions of the epilogue
-  __shared__ __attribute__((aligned(16))) uint16_t lds[4 * kOperandLds];
+  // two buffers of both operand slices, separate arrays so that stores into
+  // one can be scheduled among the reads of the other; after the products,
+  // rows 0-127 of the rounded tile go into the first, rows 128-255 into the
+  // second
+  __shared__ __attribute__((aligned(16))) uint16_t lds0[2 * kOperandLds];
+  __shared__ __attribute__((aligned(16))) uint16_t lds1[2 * kOperandLds];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   // Workgroups are dealt to the 8 XCDs in turn (workgroup i to XCD i % 8):
@@ -196,8 +199,8 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   Slice sa[kStaging], sb[kStaging];
   sa[0].load(ra, P.K, 0);
   sb[0].load(rb, P.K, 0);
-  sa[0].store(lds);
-  sb[0].store(lds + kOperandLds);
+  sa[0].store(lds0);
+  sb[0].store(lds0 + kOperandLds);
   if constexpr (kStaging == 2) {
     sa[1].load(ra, P.K, kBK);
     sb[1].load(rb, P.K, kBK);
@@ -209,12 +212,11 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   // its set into the other buffer, which was last read before the previous
   // barrier (after the last slice it is stored into the buffer no one reads
   // again).
-  auto slice = [&](const int kt, Slice& la, Slice& lb, const Slice& ka, const Slice& kb) {
+  auto slice = [&](const int kt, const uint16_t* As, uint16_t* nxt, Slice& la, Slice& lb,
+                   const Slice& ka, const Slice& kb) {
     // la/lb receive slice kt + kStaging; ka/kb hold slice kt + 1 (the same
     // sets when kStaging is 1: loaded at the top, stored at the bottom)
-    const uint16_t* As = lds + (kt & 1) * 2 * kOperandLds;
     const uint16_t* Bs = As + kOperandLds;
-    uint16_t* nxt = lds + ((kt + 1) & 1) * 2 * kOperandLds;
     la.load(ra, P.K, (kt + kStaging) * kBK);
     lb.load(rb, P.K, (kt + kStaging) * kBK);
     // A fragments are reloaded for the next 16-deep step as soon as the four
@@ -243,42 +245,32 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
     ka.store(nxt);
     kb.store(nxt + kOperandLds);
     // instruction order of the slice: the first fragments; then per step
-    // four products, then two fragment reads for the next step, four times
-    // (the global loads spread over the first step's products); the stores
-    // of the next slice over the last step's products
+    // four rounds of (two products, a global load, a product, an LDS store of
+    // the next slice, a product, two fragment reads for the next step), so
+    // the global loads and the stores spread evenly over the slice
     __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    }
-#pragma unroll
     for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i < 12) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
     __syncthreads();
   };
   if constexpr (kStaging == 1) {
-    for (int kt = 0; kt < nk; ++kt) slice(kt, sa[0], sb[0], sa[0], sb[0]);
+    for (int kt = 0; kt < nk; kt += 2) {
+      slice(kt, lds0, lds1, sa[0], sb[0], sa[0], sb[0]);
+      if (kt + 1 < nk) slice(kt + 1, lds1, lds0, sa[0], sb[0], sa[0], sb[0]);
+    }
   } else {
     // an odd count of slices gets one more, of zeros (every vector of it is
     // past the range), which adds nothing to the products
     for (int kt = 0; kt < nk; kt += 2) {
-      slice(kt, sa[0], sb[0], sa[1], sb[1]);
-      slice(kt + 1, sa[1], sb[1], sa[0], sb[0]);
+      slice(kt, lds0, lds1, sa[0], sb[0], sa[1], sb[1]);
+      slice(kt + 1, lds1, lds0, sa[1], sb[1], sa[0], sb[0]);
     }
   }
 
@@ -287,7 +279,11 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   // the tile. The rounded tile goes through LDS (the operand buffers are free
   // now): stored from there in 16-byte vectors along rows, and read back one
   // row per thread for the statistics, so no value crosses lanes.
-  uint16_t* tile = lds;                                   // [kBM][kTilePitch]
+  // tile row R lives in row R % 128 of the first (R < 128) or second array
+  auto tile_row = [&](int row) -> uint16_t* {
+    return (row < kBM / 2 ? lds0 : lds1) + (row & (kBM / 2 - 1)) * kTilePitch;
+  };
+  uint16_t* mine = wm == 0 ? lds0 : lds1;                 // this wavefront's 128 rows
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -295,8 +291,8 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
       const int col = wn * 128 + b * 32 + lr;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        tile[row * kTilePitch + col] = to_bf16(acc[a][b][r]);
+        const int row = a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        mine[row * kTilePitch + col] = to_bf16(acc[a][b][r]);
       }
     }
   __syncthreads();
@@ -310,30 +306,28 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
     typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
     const int c8 = 8 * (tid & 31);
     if (c8 < cols) {                                      // cols is a multiple of 8 here
-      const uint16_t* src = tile + (tid >> 5) * kTilePitch + c8;
       uint16_t* dst = out + static_cast<size_t>(tid >> 5) * P.N + c8;
       const size_t step = static_cast<size_t>(8) * P.N;
 #pragma unroll 8
       for (int row = tid >> 5; row < rows; row += 8) {
-        __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(src),
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(tile_row(row) + c8),
                                     reinterpret_cast<u32x4*>(dst));
-        src += 8 * kTilePitch;
         dst += step;
       }
     }
   } else {
     for (int e = tid; e < kBM * kBN; e += kThreads) {
       const int row = e >> 8, c = e & 255;
-      if (row < rows && c < cols) out[static_cast<size_t>(row) * P.N + c] = tile[row * kTilePitch + c];
+      if (row < rows && c < cols) out[static_cast<size_t>(row) * P.N + c] = tile_row(row)[c];
     }
   }
   // statistics of row tid over the tile's columns
   if (tid < rows) {
     float m, sum;
     if (cols == kBN) {
-      row_stats<kBN>(tile + tid * kTilePitch, kBN, P.k32, m, sum);
+      row_stats<kBN>(tile_row(tid), kBN, P.k32, m, sum);
     } else {
-      row_stats<0>(tile + tid * kTilePitch, cols, P.k32, m, sum);
+      row_stats<0>(tile_row(tid), cols, P.k32, m, sum);
     }
     const int row = m0 + tid;
     P.part_max[static_cast<size_t>(row) * P.tiles_n + tn] = m;
