@@ -211,54 +211,77 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   // vector is past the range and reads zeros) and slice kt + 1 is stored from
   // its set into the other buffer, which was last read before the previous
   // barrier (after the last slice it is stored into the buffer no one reads
-  // again).
+  // again). The barrier comes after the third of the four 16-deep steps, so
+  // the first fragments of slice kt + 1 are read during the fourth.
+  // Fragments: A single buffered (reloaded as soon as the four products that
+  // read it are issued), B double buffered. The first fragments of slice 0:
+  bf16x8 fa[4], fb[2][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) fa[a] = frag(lds0, fra + a * 32 * kLds);
+#pragma unroll
+  for (int b = 0; b < 4; ++b) fb[0][b] = frag(lds0 + kOperandLds, frb + b * 32 * kLds);
   auto slice = [&](const int kt, const uint16_t* As, uint16_t* nxt, Slice& la, Slice& lb,
                    const Slice& ka, const Slice& kb) {
     // la/lb receive slice kt + kStaging; ka/kb hold slice kt + 1 (the same
-    // sets when kStaging is 1: loaded at the top, stored at the bottom)
+    // sets when kStaging is 1: loaded at the top, stored before the barrier)
     const uint16_t* Bs = As + kOperandLds;
     la.load(ra, P.K, (kt + kStaging) * kBK);
     lb.load(rb, P.K, (kt + kStaging) * kBK);
-    // A fragments are reloaded for the next 16-deep step as soon as the four
-    // products that read them are issued; B fragments are double buffered
-    bf16x8 fa[4], fb[2][4];
+    // steps 0-2: products, with the fragments of the next step read from this
+    // slice's buffer and slice kt + 1 stored into the other buffer
 #pragma unroll
-    for (int a = 0; a < 4; ++a) fa[a] = frag(As, fra + a * 32 * kLds);
-#pragma unroll
-    for (int b = 0; b < 4; ++b) fb[0][b] = frag(Bs, frb + b * 32 * kLds);
-#pragma unroll
-    for (int s = 0; s < kBK / 16; ++s) {
+    for (int s = 0; s < kBK / 16 - 1; ++s) {
       const int cur = s & 1;
-      const bool next = s + 1 < kBK / 16;
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
 #pragma unroll
         for (int b = 0; b < 4; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[cur][b], acc[a][b],
                                                               0, 0, 0);
-        if (next) {
-          fa[a] = frag(As, fra + a * 32 * kLds + 16 * (s + 1));
-          fb[cur ^ 1][a] = frag(Bs, frb + a * 32 * kLds + 16 * (s + 1));
-        }
+        fa[a] = frag(As, fra + a * 32 * kLds + 16 * (s + 1));
+        fb[cur ^ 1][a] = frag(Bs, frb + a * 32 * kLds + 16 * (s + 1));
       }
     }
     ka.store(nxt);
     kb.store(nxt + kOperandLds);
-    // instruction order of the slice: the first fragments; then per step
-    // four rounds of (two products, a global load, a product, an LDS store of
-    // the next slice, a product, two fragment reads for the next step), so
-    // the global loads and the stores spread evenly over the slice
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    // instruction order before the barrier: rounds of (a product, a global
+    // load, a product, an LDS store of the next slice, a product, two
+    // fragment reads), so the loads and the stores spread over the products
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       if (i < 12) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
+    // Every wave has stored its part of slice kt + 1 and read the last
+    // fragments it needs from this slice's buffer: after the barrier, the
+    // other buffer holds slice kt + 1, and this one may be overwritten (by
+    // the stores of slice kt + 2, during the next slice's steps 0-2).
     __syncthreads();
+    // step 3: the last products of this slice, with the first fragments of
+    // slice kt + 1 read from the other buffer meanwhile
+    {
+      constexpr int s = kBK / 16 - 1;
+      constexpr int cur = s & 1;
+      static_assert(cur == 1, "step 3 hands fa and fb[0] to the next slice");
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[cur][b], acc[a][b],
+                                                              0, 0, 0);
+        fa[a] = frag(nxt, fra + a * 32 * kLds);
+        fb[cur ^ 1][a] = frag(nxt + kOperandLds, frb + a * 32 * kLds);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+    }
   };
   if constexpr (kStaging == 1) {
     for (int kt = 0; kt < nk; kt += 2) {
@@ -273,6 +296,7 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
       slice(kt + 1, lds1, lds0, sa[1], sb[1], sa[0], sb[0]);
     }
   }
+  __syncthreads();   // the last fragment reads are done before the tile overwrites the buffers
 
   // Epilogue. Accumulator r of block (a, b) holds row
   // 128 wm + 32 a + 8 (r / 4) + 4 lh + r % 4 and column 128 wn + 32 b + lr of
