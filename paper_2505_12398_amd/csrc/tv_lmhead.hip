@@ -20,11 +20,11 @@
 // the hidden states and of the weight once from HBM and share it through the
 // XCD's L2.
 //
-// Epilogue. Each accumulator is rounded to bf16 (round to nearest even) into
-// the tile in LDS; the tile is stored in 16-byte vectors along its rows; then
-// each thread reads one row of it back and forms the row's maximum and its sum
-// of 2^((z - max) k), k = log2(e)/T, in fp32: one (max, sum) partial per row
-// and column tile. A second kernel merges a row's partials in fp64 (exact
+// Epilogue. Each accumulator is rounded to bf16 (round to nearest even, by the
+// hardware conversion) into the tile in LDS; the tile is stored in 16-byte
+// vectors along its rows; then each thread reads one row of it back and forms
+// the row's maximum and its sum of 2^((z - max) k), k = log2(e)/T, in fp32:
+// one (max, sum) partial per row and column tile. A second kernel merges a row's partials in fp64 (exact
 // power-of-two rescaling of each partial to the row maximum).
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -60,17 +60,6 @@ struct LmParams {
   int M, K, N, tiles_n;
   float k32;              // log2(e) / T rounded to fp32
 };
-
-// fp32 -> bf16 bits, round to nearest even (NaN kept quiet)
-__device__ __forceinline__ uint16_t to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-  const uint32_t quiet = (u >> 16) | 0x40u;
-  return static_cast<uint16_t>((u & 0x7fffffffu) > 0x7f800000u ? quiet : rounded);
-}
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
-  return __uint_as_float(static_cast<uint32_t>(b) << 16);
-}
 
 // One K-slice of a 256-row operand tile: 2048 16-byte vectors, eight per
 // thread (vector v = thread + 256 q: row v / 8, 8 bf16 at column 8 (v % 8)).
@@ -316,7 +305,8 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        mine[row * kTilePitch + col] = to_bf16(acc[a][b][r]);
+        // the hardware conversion (v_cvt_pk_bf16_f32) rounds to nearest even
+        mine[row * kTilePitch + col] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(acc[a][b][r]));
       }
     }
   __syncthreads();

@@ -80,6 +80,29 @@ def test_lmhead_ragged_tiles(M, K, N, T):
           f"{same:.4f} equal to the rounded exact value, stats rel err {rel:.2e}", flush=True)
 
 
+def test_lmhead_rounding_is_nearest_even():
+    """Integer inputs whose products and fp32 sums are exact (|sum| < 2^24),
+    with sums of up to 13 significant bits: the bf16 rounding is then the only
+    rounding, and every logit must be the exact sum rounded to nearest even
+    (torch's float32 -> bfloat16 conversion), bit for bit. Ties occur (sums
+    with 9 significant bits whose last is 1) and must round to even."""
+    M, K, N = 130, 96, 515
+    g = torch.Generator(device="cpu").manual_seed(41)
+    x = torch.randint(-12, 13, (M, K), generator=g).float()
+    w = torch.randint(-12, 13, (N, K), generator=g).float()
+    z, _, _ = tv.lmhead_stats(x.to(DEV).to(torch.bfloat16), w.to(DEV).to(torch.bfloat16), 1.0)
+    torch.cuda.synchronize()
+    exact = x.double() @ w.double().T
+    assert exact.abs().max() < 2 ** 24
+    want = exact.float().to(torch.bfloat16)
+    got = z.cpu()
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16)), \
+        int((got.view(torch.int16) != want.view(torch.int16)).sum())
+    ties = int(((exact.abs().long() % 2 == 1) & (exact.abs() >= 256) & (exact.abs() < 512)).sum())
+    print(f"lmhead rounding: {M * N} logits equal to the nearest-even rounding, {ties} ties", flush=True)
+    assert ties > 0
+
+
 def test_lmhead_benchmark_shape_sampled_rows():
     """The benchmark's shape: 16640 rows (256 trees x 65 nodes), hidden 4096,
     V = 128256; 24 sampled rows checked against the exact products, every
