@@ -108,36 +108,41 @@ constexpr int kTilePitch = kBN + 8;           // bf16 elements per row of the ro
 static_assert((kBM / 2) * kTilePitch <= 2 * kOperandLds, "half the rounded tile fits a buffer");
 
 // Statistics of one row of the rounded tile in LDS over its first `cols`
-// columns (kCols > 0: all kCols, with no masking): the maximum, then the sum
-// of 2^((z - max) k) in fp32. The hardware exp2 gives 0 for -inf, so a row
-// whose columns are all -inf sums 0; NaN or +inf propagate into the sum (NaN
-// is not ordered by fmaxf and surfaces there).
+// columns (kCols > 0: all kCols, with no masking), in one pass: the running
+// maximum m and the sum of 2^(z k + c) in the frame c = -m k (fp32 product);
+// when a group of 8 values raises the maximum, the partial sums move to the
+// new frame by 2^(c_new - c_old). At the end the frame is that of the row's
+// maximum, as if the terms had been formed with it. The hardware exp2 gives 0
+// for -inf, so a row whose columns are all -inf sums 0 (its frame never
+// moves); NaN or +inf propagate into the sum (NaN is not ordered by fmaxf and
+// surfaces there; +inf makes the frame -inf and its term NaN).
 template <int kCols>
 __device__ __forceinline__ void row_stats(const uint16_t* tr, int cols, float k, float& m_out,
                                           float& s_out) {
-  float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-#pragma unroll 8
-  for (int j = 0; j < kBN / 8; ++j) {
-    const uint4 q = *reinterpret_cast<const uint4*>(tr + 8 * j);
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float z = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
-      if (kCols > 0 || 8 * j + e < cols) mx[e & 3] = fmaxf(mx[e & 3], z);
-    }
-  }
-  const float m = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
-  const float c = (m > -INFINITY) ? -m * k : 0.0f;
+  float m = -INFINITY, c = 0.0f;
   float sm[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 8
+#pragma unroll 4
   for (int j = 0; j < kBN / 8; ++j) {
     const uint4 q = *reinterpret_cast<const uint4*>(tr + 8 * j);
     const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    float z[8];
+    float gm = -INFINITY;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float z = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
-      if (kCols > 0 || 8 * j + e < cols) sm[e & 3] += __builtin_amdgcn_exp2f(fmaf(z, k, c));
+      z[e] = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
+      if (kCols == 0 && 8 * j + e >= cols) z[e] = -INFINITY;
+      gm = fmaxf(gm, z[e]);
     }
+    if (gm > m) {
+      const float cn = -gm * k;
+      const float f = m > -INFINITY ? __builtin_amdgcn_exp2f(cn - c) : 1.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sm[i] *= f;
+      m = gm;
+      c = cn;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sm[e & 3] += __builtin_amdgcn_exp2f(fmaf(z[e], k, c));
   }
   m_out = m;
   s_out = (sm[0] + sm[1]) + (sm[2] + sm[3]);
