@@ -213,3 +213,55 @@ def test_lmhead_then_verify_stats_pipeline():
     assert not rep.failures, "\n".join(rep.failures[:10])
     assert rep.near_ties <= 1
     assert rep.max_theta_abs < parity.BAND, rep.summary()
+
+
+@pytest.mark.parametrize("cfg,vocab", [(2, None), (3, 4099), (4, 20000)])
+@pytest.mark.parametrize("mode", [W.WITHOUT_REPLACEMENT, W.WITH_REPLACEMENT])
+def test_verify_stats_other_workloads(cfg, vocab, mode):
+    """tv_verify_stats with the oracle's row statistics on the other workloads:
+    the precise element path (fp32 logits of the chain workload; bf16 logits
+    below 16384 tokens, the binary-tree workload at V = 4099, T = 0.7) and the
+    fast one on the irregular workload at V = 20000; every tree against the
+    oracle, with theta (no early rejection) and without."""
+    bt = W.make_batch(cfg, step=17, device=DEV, mode=mode, vocab=vocab)
+    stats, host = _stats_np(bt)
+    B = bt["parents"].shape[0]
+    refs = parity.oracle_many(bt, range(B), tokenlevels=(False,), host=host)[False]
+    for theta in (True, False):
+        g = parity.host_outputs(tv.verify_batch(
+            bt["parents"], bt["tokens"], bt["target"], bt["draft"], bt["temperature"],
+            bt["uniforms"], mode, want_theta=theta, want_p_init=theta, stats=stats))
+        rep = parity.check(bt, False, trees=list(range(B)), refs=refs, gpu=g, theta=theta,
+                           p_init=theta, label=f"verify_stats cfg{cfg} mode={mode} theta={theta}")
+        print(f"verify_stats cfg{cfg} V={bt['target'].shape[-1]} mode={mode} theta={theta}: "
+              f"{rep.summary()}", flush=True)
+        assert not rep.failures, "\n".join(rep.failures[:10])
+        assert rep.near_ties <= max(1, B // 100)
+
+
+def test_verify_stats_bad_statistics():
+    """Statistics that cannot normalise a consulted row (the root's, which every
+    tree with children consults): a NaN target sum, a zero draft sum, an
+    infinite target maximum, a -inf draft maximum. Each such tree reports
+    TV_TREE_NONFINITE with the sentinel outputs; the other trees of the launch
+    match the oracle."""
+    bt = W.make_batch(5, step=21, device=DEV, mode=W.WITHOUT_REPLACEMENT, batch=8, vocab=32768)
+    stats, host = _stats_np(bt)
+    tmax, tsum, dmax, dsum = [s.clone() for s in stats]
+    tsum[1, 0] = float("nan")
+    dsum[2, 0] = 0.0
+    tmax[3, 0] = float("inf")
+    dmax[4, 0] = float("-inf")
+    g = parity.host_outputs(tv.verify_batch(
+        bt["parents"], bt["tokens"], bt["target"], bt["draft"], bt["temperature"],
+        bt["uniforms"], bt["mode"], want_theta=True, want_p_init=True,
+        stats=(tmax, tsum, dmax, dsum)))
+    for b in (1, 2, 3, 4):
+        assert g["status"][b] == tv.TV_TREE_NONFINITE, (b, g["status"][b])
+        assert g["accept_len"][b] == -1 and g["accepted_node"][b] == -1
+        assert g["bonus_token"][b] == -1
+    good = [0, 5, 6, 7]
+    refs = parity.oracle_many(bt, good, tokenlevels=(False,), host=host)[False]
+    rep = parity.check(bt, False, trees=good, refs=refs, gpu=g, theta=True, p_init=True,
+                       label="verify_stats bad statistics")
+    assert not rep.failures, "\n".join(rep.failures[:10])
