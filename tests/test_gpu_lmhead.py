@@ -103,6 +103,26 @@ def test_lmhead_rounding_is_nearest_even():
     assert ties > 0
 
 
+def test_lmhead_misaligned_logits():
+    """Logits written into a buffer that starts 2 bytes past a 16-byte
+    boundary (the element-by-element store path), N a multiple of 8: equal bit
+    for bit to the same call into an aligned buffer, statistics included."""
+    M, K, N = 300, 136, 1024
+    g = torch.Generator(device=DEV).manual_seed(17)
+    x = torch.randn((M, K), generator=g, device=DEV).to(torch.bfloat16)
+    w = (torch.randn((N, K), generator=g, device=DEV) * 0.3).to(torch.bfloat16)
+    z0, m0, s0 = tv.lmhead_stats(x, w, 0.9)
+    flat = torch.zeros(M * N + 1, dtype=torch.bfloat16, device=DEV)
+    z1 = flat[1:].view(M, N)
+    assert z1.data_ptr() % 16 == 2
+    out = (z1, torch.empty(M, device=DEV), torch.empty(M, dtype=torch.float64, device=DEV))
+    tv.lmhead_stats(x, w, 0.9, out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(z1.view(torch.int16), z0.view(torch.int16))
+    assert torch.equal(out[1], m0) and torch.equal(out[2], s0)
+    assert flat[0].item() == 0.0      # nothing written before the buffer
+
+
 def test_lmhead_benchmark_shape_sampled_rows():
     """The benchmark's shape: 16640 rows (256 trees x 65 nodes), hidden 4096,
     V = 128256; 24 sampled rows checked against the exact products, every
