@@ -2373,7 +2373,7 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   __shared__ WgScratch ws_;
   Lds<SampleSmem>& sm = lds_ref(sm_);
   Lds<WgScratch>& ws = lds_ref(ws_);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int n1 = S.num_nodes;
   const int b = static_cast<int>(blockIdx.x / static_cast<unsigned>(n1));
   const int j = static_cast<int>(blockIdx.x - static_cast<unsigned>(b) * n1);

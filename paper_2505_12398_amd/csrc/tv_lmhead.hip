@@ -10,9 +10,10 @@
 // v_mfma_f32_32x32x16_bf16 (fp32 accumulation, 256 accumulator registers per
 // lane, one wavefront per SIMD). K advances 64 at a time through two LDS
 // buffers: while the products of one K-slice are formed from one buffer, the
-// next slice of both operand tiles is loaded from global memory into
-// registers (16-byte loads, coalesced along K) and then stored into the other
-// buffer, so one barrier per K-slice suffices. Both operands are K-contiguous
+// slice after next of both operand tiles is loaded from global memory into
+// registers (16-byte loads, coalesced along K) and the next one is stored
+// into the other buffer, so one barrier per K-slice suffices; the loads and
+// stores are spread evenly over the products. Both operands are K-contiguous
 // (hidden [M][K], weight [N][K]), so every MFMA operand fragment is one
 // 16-byte LDS read; LDS rows are padded by 16 bytes against bank conflicts.
 // Each XCD gets a contiguous run of tiles, ordered in bands of 8 row tiles
@@ -24,8 +25,8 @@
 // hardware conversion) into the tile in LDS; the tile is stored in 16-byte
 // vectors along its rows; then each thread reads one row of it back and forms
 // the row's maximum and its sum of 2^((z - max) k), k = log2(e)/T, in fp32:
-// one (max, sum) partial per row and column tile. A second kernel merges a row's partials in fp64 (exact
-// power-of-two rescaling of each partial to the row maximum).
+// one (max, sum) partial per row and column tile. A second kernel merges a
+// row's partials in fp64, each moved to the frame of the row maximum.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -40,10 +41,6 @@ constexpr int kLds = kBK + 8;          // padded LDS row, bf16 elements (144 byt
 constexpr int kThreads = 256;
 constexpr int kGroupM = 8;             // row tiles per band of the tile order
 constexpr int kVecs = kBM * kBK / 8 / kThreads;   // 16-byte vectors per thread and operand
-#ifndef TV_LMHEAD_STAGING
-#define TV_LMHEAD_STAGING 2
-#endif
-constexpr int kStaging = TV_LMHEAD_STAGING;        // register sets of operand slices in flight
 static_assert(kBM == kBN, "one load pattern serves both operands");
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -187,21 +184,18 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   const int nk = (P.K + kBK - 1) / kBK;
   const int fra = (wm * 128 + lr) * kLds + 8 * lh;      // this lane's fragment offsets
   const int frb = (wn * 128 + lr) * kLds + 8 * lh;
-  // kStaging register sets of slices: with two, slice kt + 1 waits in one
-  // while slice kt + 2 is loaded into the other, so a load has two slices'
-  // products to arrive; with one, a load has one.
-  Slice sa[kStaging], sb[kStaging];
+  // Two register sets of slices: slice kt + 1 waits in one while slice
+  // kt + 2 is loaded into the other.
+  Slice sa[2], sb[2];
   sa[0].load(ra, P.K, 0);
   sb[0].load(rb, P.K, 0);
   sa[0].store(lds0);
   sb[0].store(lds0 + kOperandLds);
-  if constexpr (kStaging == 2) {
-    sa[1].load(ra, P.K, kBK);
-    sb[1].load(rb, P.K, kBK);
-  }
+  sa[1].load(ra, P.K, kBK);
+  sb[1].load(rb, P.K, kBK);
   __syncthreads();
   // One K-slice: the products of slice kt from LDS buffer kt % 2 while slice
-  // kt + kStaging is loaded into a register set (beyond the last slice every
+  // kt + 2 is loaded into a register set (beyond the last slice every
   // vector is past the range and reads zeros) and slice kt + 1 is stored from
   // its set into the other buffer, which was last read before the previous
   // barrier (after the last slice it is stored into the buffer no one reads
@@ -216,11 +210,10 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
   for (int b = 0; b < 4; ++b) fb[0][b] = frag(lds0 + kOperandLds, frb + b * 32 * kLds);
   auto slice = [&](const int kt, const uint16_t* As, uint16_t* nxt, Slice& la, Slice& lb,
                    const Slice& ka, const Slice& kb) {
-    // la/lb receive slice kt + kStaging; ka/kb hold slice kt + 1 (the same
-    // sets when kStaging is 1: loaded at the top, stored before the barrier)
+    // la/lb receive slice kt + 2; ka/kb hold slice kt + 1
     const uint16_t* Bs = As + kOperandLds;
-    la.load(ra, P.K, (kt + kStaging) * kBK);
-    lb.load(rb, P.K, (kt + kStaging) * kBK);
+    la.load(ra, P.K, (kt + 2) * kBK);
+    lb.load(rb, P.K, (kt + 2) * kBK);
     // steps 0-2: products, with the fragments of the next step read from this
     // slice's buffer and slice kt + 1 stored into the other buffer
 #pragma unroll
@@ -277,18 +270,11 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
       }
     }
   };
-  if constexpr (kStaging == 1) {
-    for (int kt = 0; kt < nk; kt += 2) {
-      slice(kt, lds0, lds1, sa[0], sb[0], sa[0], sb[0]);
-      if (kt + 1 < nk) slice(kt + 1, lds1, lds0, sa[0], sb[0], sa[0], sb[0]);
-    }
-  } else {
-    // an odd count of slices gets one more, of zeros (every vector of it is
-    // past the range), which adds nothing to the products
-    for (int kt = 0; kt < nk; kt += 2) {
-      slice(kt, lds0, lds1, sa[0], sb[0], sa[1], sb[1]);
-      slice(kt + 1, lds1, lds0, sa[1], sb[1], sa[0], sb[0]);
-    }
+  // an odd count of slices gets one more, of zeros (every vector of it is
+  // past the range), which adds nothing to the products
+  for (int kt = 0; kt < nk; kt += 2) {
+    slice(kt, lds0, lds1, sa[0], sb[0], sa[1], sb[1]);
+    slice(kt + 1, lds1, lds0, sa[1], sb[1], sa[0], sb[0]);
   }
   __syncthreads();   // the last fragment reads are done before the tile overwrites the buffers
 
@@ -355,7 +341,8 @@ __global__ void __launch_bounds__(kThreads) lmhead_kernel(LmParams P) {
 }
 
 // Merges the column-tile partials of one row per wavefront (fp64 sum, each
-// partial rescaled to the row maximum by an exact power of two).
+// partial moved from its frame to the row maximum's by 2^(frame difference),
+// evaluated in fp64).
 __global__ void __launch_bounds__(kThreads) lmhead_merge_kernel(LmParams P) {
   const int lane = threadIdx.x & 63;
   const int row = static_cast<int>(blockIdx.x) * (kThreads / 64) + (threadIdx.x >> 6);
@@ -367,7 +354,7 @@ __global__ void __launch_bounds__(kThreads) lmhead_merge_kernel(LmParams P) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
   // each partial is in the frame -max_t * k (an fp32 product): move it to the
-  // row's frame -m * k by the exact power of two between the two frames
+  // row's frame -m * k by 2 to the difference of the two frames
   const double cm = static_cast<double>(-m * P.k32);
   double s = 0.0;
   for (int t = lane; t < P.tiles_n; t += 64) {
