@@ -2379,21 +2379,28 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   const int j = static_cast<int>(blockIdx.x - static_cast<unsigned>(b) * n1);
   const int32_t* par = S.parents + static_cast<size_t>(b) * n1;
 
-  // the tree's links (every row checks them) and this node's children in order
+  // the tree's links (every row checks them) and whether this node has
+  // children: a row without children (about half of them) stops here
+  int bad = 0, anykid = 0;
+  for (int i = tid; i < n1; i += kNT) {
+    const int p = par[i];
+    if (i == 0 ? p != -1 : (p < 0 || p >= i)) bad = 1;
+    if (i > 0 && p == j) anykid = 1;
+  }
+  if (__syncthreads_or(bad)) {
+    if (j == 0 && tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_BAD_PARENT));
+    return;
+  }
+  if (!__syncthreads_or(anykid)) return;
+  // the children in order
   if (tid == 0) {
     sm.nkids = 0;
     sm.nremoved = 0;
   }
   __syncthreads();
-  int bad = 0;
   for (int base = 0; base < n1; base += kNT) {
     const int i = base + tid;
-    int p = -2;
-    if (i < n1) {
-      p = par[i];
-      if (i == 0 ? p != -1 : (p < 0 || p >= i)) bad = 1;
-    }
-    const bool kid = i < n1 && i > 0 && p == j;
+    const bool kid = i < n1 && i > 0 && par[i] == j;
     const double inc = block_incl_scan(ws, kid ? 1.0 : 0.0);
     const int before = sm.nkids;
     if (kid) sm.kids[before + static_cast<int>(inc) - 1] = i;
@@ -2401,13 +2408,7 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
     if (tid == kNT - 1) sm.nkids = before + static_cast<int>(inc);
     __syncthreads();
   }
-  bad = __syncthreads_or(bad);
-  if (bad) {
-    if (j == 0 && tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_BAD_PARENT));
-    return;
-  }
   const int nk = sm.nkids;
-  if (nk == 0) return;
 
   const T* row = static_cast<const T*>(S.draft) + (static_cast<size_t>(b) * n1 + j) *
                                                       static_cast<size_t>(S.vocab);
@@ -2429,8 +2430,9 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   // are summed; a chunk keeps the frame of its running maximum (Online). No
   // reduction across threads until the row is read. A chunk's sum is the
   // fp64 sum of fp32 sums of 8 units on the fast path (fp64 terms on the
-  // precise one): relative error about 64 * 2^-24 of the chunk's sum, hence
-  // of the row's total W, below the 1e-6 * W near-tie band.
+  // precise one), moved into the row's frame by an fp32 factor on the fast
+  // path: relative error about 66 * 2^-24 of the chunk's sum, hence of the
+  // row's total W, below the 1e-6 * W near-tie band.
   const int nsb = cu / 8;                        // 8-unit blocks per chunk
   const int my_chunks = C > tid ? (C - tid + kNT - 1) / kNT : 0;
   const int items = my_chunks * nsb;
@@ -2514,7 +2516,13 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   for (int c = cb; c < ce; ++c) {
     const float M = sm.cm[c];
     double v = sm.cs[c];
-    if (M > -INFINITY) v *= exp2(cf - ar.frame(M));
+    if (M > -INFINITY) {
+      if constexpr (A::kPrecise) {
+        v *= exp2(cf - ar.frame(M));
+      } else {   // fp32 factor (the chunk sums carry fp32 rounding already)
+        v *= static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(cf - ar.frame(M))));
+      }
+    }
     if (!isfinite(v)) nonfinite = 1;
     sm.cs[c] = v;
     ts += v;
