@@ -234,6 +234,13 @@ template <> struct Elem<uint16_t> {          // bfloat16 bit patterns
   __device__ static inline float scalar(const uint16_t* p) {
     return __uint_as_float(static_cast<uint32_t>(*p) << 16);
   }
+  // a value of the row (or an infinity) back into its own format, exactly
+  __device__ static inline uint16_t narrow(float x) {
+    return static_cast<uint16_t>(__float_as_uint(x) >> 16);
+  }
+  __device__ static inline float widen(uint16_t v) {
+    return __uint_as_float(static_cast<uint32_t>(v) << 16);
+  }
 };
 
 template <> struct Elem<float> {
@@ -243,6 +250,8 @@ template <> struct Elem<float> {
     x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
   }
   __device__ static inline float scalar(const float* p) { return *p; }
+  __device__ static inline float narrow(float x) { return x; }
+  __device__ static inline float widen(float v) { return v; }
 };
 
 // A row split into a scalar head (up to the first 16-byte boundary), full
@@ -2257,13 +2266,34 @@ struct SampleParams {
 // (2^17 vectors plus 14 head and tail elements)
 constexpr int kSampleMaxChunks = 2056;
 
+// The sampler's frames are integers: c(m) = -ceil(m k), so that a sum moves
+// from one frame to another by an exact power of two. Terms stay at most 1
+// and the fp32 frame is exact (an integer-valued fp32 on the fast path).
+template <class A>
+__device__ __forceinline__ double sample_frame(const A& ar, float m) {
+  if constexpr (A::kPrecise) return -ceil(static_cast<double>(m) * ar.k);
+  else return static_cast<double>(-ceilf(m * ar.k));
+}
+
+// v * 2^d for a frame difference d <= 0 (exact unless the result underflows)
+__device__ __forceinline__ double frame_shift(double v, double d) {
+  return ldexp(v, static_cast<int>(fmax(d, -4096.0)));
+}
+
+template <typename T>
 struct SampleSmem {
   double cs[kSampleMaxChunks];     // chunk weight sums, in the row's frame once rescaled
-  float cm[kSampleMaxChunks];      // chunk maxima
+  T cm[kSampleMaxChunks];          // chunk maxima, values of the row in its element format
   int32_t kids[TV_MAX_NODES];      // children of the row's node, ascending
   int32_t removed[TV_MAX_NODES];   // tokens drawn so far at this row (without replacement)
   int nkids, nremoved, owner, chunk, token;
   double W, run;
+};
+
+// the workgroup reductions' scratch, without the verifier's fields
+struct SampleScratch {
+  float red_f[2 * kNW];
+  double scan_d[kNW];
 };
 
 // Every tree starts OK with the root's token -1; the rows then raise status.
@@ -2296,7 +2326,7 @@ struct RowWeights {
   const T* row;
   Geom g;
   A ar;
-  const Lds<SampleSmem>* sm;
+  const Lds<SampleSmem<T>>* sm;
 
   __device__ int units() const { return g.head + g.nvec + g.tail; }
   __device__ int first(int u) const {
@@ -2369,10 +2399,10 @@ struct RowWeights {
 
 template <typename T, class A>
 __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
-  __shared__ SampleSmem sm_;
-  __shared__ WgScratch ws_;
-  Lds<SampleSmem>& sm = lds_ref(sm_);
-  Lds<WgScratch>& ws = lds_ref(ws_);
+  __shared__ SampleSmem<T> sm_;
+  __shared__ SampleScratch ws_;
+  Lds<SampleSmem<T>>& sm = lds_ref(sm_);
+  Lds<SampleScratch>& ws = lds_ref(ws_);
   const int tid = threadIdx.x, lane = tid & 63;
   const int n1 = S.num_nodes;
   const int b = static_cast<int>(blockIdx.x / static_cast<unsigned>(n1));
@@ -2429,10 +2459,9 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   // ends of the row), the next 8 units' loads in flight while the current ones
   // are summed; a chunk keeps the frame of its running maximum (Online). No
   // reduction across threads until the row is read. A chunk's sum is the
-  // fp64 sum of fp32 sums of 8 units on the fast path (fp64 terms on the
-  // precise one), moved into the row's frame by an fp32 factor on the fast
-  // path: relative error about 66 * 2^-24 of the chunk's sum, hence of the
-  // row's total W, below the 1e-6 * W near-tie band.
+  // fp64 sum of its units' sums, each of those formed as the draw's rescan
+  // forms it (fp32 terms added in fp32 on the fast path, fp64 on the precise
+  // one), and is moved into the row's frame by an fp64 factor.
   const int nsb = cu / 8;                        // 8-unit blocks per chunk
   const int my_chunks = C > tid ? (C - tid + kNT - 1) / kNT : 0;
   const int items = my_chunks * nsb;
@@ -2445,56 +2474,83 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
     }
   };
   float tmax = -INFINITY;
-  Online o = online_init(ar);
+  const Online o0{-INFINITY, sample_frame(ar, kFrameSentinel), 0.0};
+  Online o = o0;
   uint4 cur[8], nxt[8];
   if (items > 0) load_block(block_unit(0), cur);
   for (int i = 0; i < items; ++i) {
     if (i + 1 < items) load_block(block_unit(i + 1), nxt);
     const int ub = block_unit(i);
-    if (i % nsb == 0) o = online_init(ar);
-    float x[8][E];
-    if (pure(ub)) {
+    if (i % nsb == 0) o = o0;
+    float vmax = -INFINITY;
+    const bool pb = pure(ub);
+    if (pb) {
+      // the values are unpacked again for the sums rather than kept: the
+      // 8 x E floats would hold registers that the loads in flight need
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         pin(cur[e]);
-        Elem<T>::unpack(cur[e], x[e]);
+        float t[E];
+        Elem<T>::unpack(cur[e], t);
+#pragma unroll
+        for (int q = 0; q < E; ++q) vmax = fmaxf(vmax, t[q]);
       }
     } else {
       for (int e = 0; e < 8; ++e) {
         if (ub + e < U) {
-          rw.load(ub + e, x[e]);
-        } else {
+          float t[E];
+          rw.load(ub + e, t);
 #pragma unroll
-          for (int q = 0; q < E; ++q) x[e][q] = -INFINITY;
+          for (int q = 0; q < E; ++q) vmax = fmaxf(vmax, t[q]);
         }
       }
     }
-    float vmax = -INFINITY;
+    if (vmax > o.m) {
+      const double cn = sample_frame(ar, vmax);
+      o.s = frame_shift(o.s, cn - o.c);
+      o.m = vmax;
+      o.c = cn;
+    }
+    // a unit's sum is formed as a rescan forms it (its terms in order, in the
+    // precision of the terms), and unit sums are added in fp64
+    const float cf32 = static_cast<float>(o.c);
+    auto add_unit = [&](const float (&t)[E]) {
+      if constexpr (A::kPrecise) {
+        double acc = 0.0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
+        for (int q = 0; q < E; ++q) acc += ar.ex(t[q], o.c);
+        o.s += acc;
+      } else {
+        float acc = 0.0f;
 #pragma unroll
-      for (int q = 0; q < E; ++q) vmax = fmaxf(vmax, x[e][q]);
-    online_raise(o, vmax, ar);
-    if constexpr (A::kPrecise) {
+        for (int q = 0; q < E; ++q) acc += fast_exp2(fmaf(t[q], ar.k, cf32));
+        o.s += static_cast<double>(acc);
+      }
+    };
+    if (pb) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-#pragma unroll
-        for (int q = 0; q < E; ++q) o.s += ar.ex(x[e][q], o.c);
+      for (int e = 0; e < 8; ++e) {
+        pin(cur[e]);
+        float t[E];
+        Elem<T>::unpack(cur[e], t);
+        add_unit(t);
+      }
     } else {
-      const float cf32 = static_cast<float>(o.c);
-      float part = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-#pragma unroll
-        for (int q = 0; q < E; ++q) part += fast_exp2(fmaf(x[e][q], ar.k, cf32));
-      o.s += static_cast<double>(part);
+      for (int e = 0; e < 8; ++e) {
+        if (ub + e < U) {
+          float t[E];
+          rw.load(ub + e, t);
+          add_unit(t);
+        }
+      }
     }
     if (i % nsb == nsb - 1) {
       const int c = tid + kNT * (i / nsb);
       // the sum in the frame of the chunk's maximum (that of the sentinel, with
-      // sum 0 or NaN, when the chunk has no finite value)
+      // sum 0 or NaN, when the chunk has no finite value); the maximum is a
+      // value of the row, kept in the row's element format
       sm.cs[c] = o.s;
-      sm.cm[c] = o.m;
+      sm.cm[c] = Elem<T>::narrow(o.m);
       tmax = fmaxf(tmax, o.m);
     }
 #pragma unroll
@@ -2506,7 +2562,7 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
     if (tid == 0) atomicMax(&S.status[b], static_cast<int32_t>(TV_TREE_NONFINITE));
     return;
   }
-  const double cf = ar.frame(rowmax);   // the row's frame
+  const double cf = sample_frame(ar, rowmax);   // the row's frame
 
   // chunk sums into the row's frame; thread t owns the chunks [cb, ce)
   const int cb = static_cast<int>(static_cast<long long>(C) * tid / kNT);
@@ -2514,14 +2570,10 @@ __global__ void __launch_bounds__(kNT) sample_kernel(SampleParams S, A ar) {
   double ts = 0.0;
   int nonfinite = 0;
   for (int c = cb; c < ce; ++c) {
-    const float M = sm.cm[c];
+    const float M = Elem<T>::widen(sm.cm[c]);
     double v = sm.cs[c];
     if (M > -INFINITY) {
-      if constexpr (A::kPrecise) {
-        v *= exp2(cf - ar.frame(M));
-      } else {   // fp32 factor (the chunk sums carry fp32 rounding already)
-        v *= static_cast<double>(__builtin_amdgcn_exp2f(static_cast<float>(cf - ar.frame(M))));
-      }
+      v = frame_shift(v, cf - sample_frame(ar, M));
     }
     if (!isfinite(v)) nonfinite = 1;
     sm.cs[c] = v;
