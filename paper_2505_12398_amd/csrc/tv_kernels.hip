@@ -1160,8 +1160,9 @@ __device__ __forceinline__ const T* row_ptr(const PP& P, const void* base, int b
 // Loads and checks tree b into LDS, gathers every node's logits at its token
 // in its parent's rows, and starts the traversal (all threads).
 template <typename T, class A, int kCap>
-__device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, const Lds<Params>& P,
-                                                     A ar, int b) {
+__device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
+                                                     const Lds<Params>& P, A ar, int b) {
+  constexpr int kPer = (kCap + kNT - 1) / kNT;   // nodes per thread
   const int tid = threadIdx.x;
   const int n1 = P.num_nodes;
   const int V = P.vocab;
@@ -1196,43 +1197,108 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, co
       __hip_atomic_fetch_add(&sm.child_count[sm.parent[i]], 1, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_WORKGROUP);
     __syncthreads();
-    if (tid == 0) {
-      int start = 0;
-      for (int j = 0; j < n1; ++j) {
-        sm.child_start[j] = static_cast<int16_t>(start);
-        start += sm.child_count[j];
+    {
+      // first child slot of every node: exclusive prefix sum of the counts,
+      // thread t summing the nodes [t q, t q + q)
+      const int q = (n1 + kNT - 1) / kNT;
+      const int lo = min(n1, tid * q), hi = min(n1, lo + q);
+      int loc = 0;
+      for (int j = lo; j < hi; ++j) loc += sm.child_count[j];
+      int run = static_cast<int>(block_incl_scan(ws, static_cast<double>(loc))) - loc;
+      for (int j = lo; j < hi; ++j) {
+        sm.child_start[j] = static_cast<int16_t>(run);
+        run += sm.child_count[j];
       }
     }
     __syncthreads();
-    // rank among siblings = earlier nodes with the same parent
+    // the children in any order (the counts, counted down, hand out the
+    // slots), then the counts again from the starts
     for (int i = 1 + tid; i < n1; i += kNT) {
       const int p = sm.parent[i];
-      int rank = 0, d = 1;
-      for (int k2 = 1; k2 < i; ++k2) rank += (sm.parent[k2] == p);
-      for (int a = p; a > 0; a = sm.parent[a]) ++d;
-      sm.child_list[sm.child_start[p] + rank] = static_cast<int16_t>(i);
-      sm.rank[i] = static_cast<int16_t>(rank);
-      sm.depth[i] = static_cast<int16_t>(d);
+      const int pos = __hip_atomic_fetch_add(&sm.child_count[p], -1, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_WORKGROUP) - 1;
+      sm.child_list[sm.child_start[p] + pos] = static_cast<int16_t>(i);
     }
-    if (tid == 0) sm.depth[0] = 0;
     __syncthreads();
+    for (int j = tid; j < n1; j += kNT)
+      sm.child_count[j] = (j + 1 < n1 ? sm.child_start[j + 1] : n1 - 1) - sm.child_start[j];
+    __syncthreads();
+    // a child's rank is the number of its siblings with smaller indices; the
+    // same scan finds a token drawn twice among siblings
+    const bool wo = P.mode == TV_SIBLINGS_WITHOUT_REPLACEMENT;
+    int rk[kPer];
     int dup = 0;
-    if (P.mode == TV_SIBLINGS_WITHOUT_REPLACEMENT) {
-      for (int i = 1 + tid; i < n1; i += kNT) {
-        const int p = sm.parent[i];
-        const int s0 = sm.child_start[p], cnt = sm.child_count[p];
-        for (int r = 0; r < cnt; ++r) {
-          const int c = sm.child_list[s0 + r];
-          if (c > i && sm.token[c] == sm.token[i]) dup = 1;
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = 1 + tid + t * kNT;
+      rk[t] = 0;
+      if (i < n1) {
+        const int p = sm.parent[i], s0 = sm.child_start[p], cnt = sm.child_count[p];
+        const int x = sm.token[i];
+        int r = 0;
+        for (int k2 = 0; k2 < cnt; ++k2) {
+          const int c = sm.child_list[s0 + k2];
+          r += c < i;
+          if (wo && c != i && sm.token[c] == x) dup = 1;
         }
+        rk[t] = r;
       }
     }
+    __syncthreads();
+    // in index order, and every node's depth (its walks to the root taken
+    // side by side)
+    int a[kPer], d[kPer];
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = 1 + tid + t * kNT;
+      a[t] = 0;
+      d[t] = 1;
+      if (i < n1) {
+        const int p = sm.parent[i];
+        sm.child_list[sm.child_start[p] + rk[t]] = static_cast<int16_t>(i);
+        sm.rank[i] = static_cast<int16_t>(rk[t]);
+        a[t] = p;
+      }
+    }
+    for (;;) {
+      bool any = false;
+#pragma unroll
+      for (int t = 0; t < kPer; ++t) {
+        if (a[t] > 0) {
+          a[t] = sm.parent[a[t]];
+          ++d[t];
+          any = true;
+        }
+      }
+      if (!any) break;
+    }
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = 1 + tid + t * kNT;
+      if (i < n1) sm.depth[i] = static_cast<int16_t>(d[t]);
+    }
+    if (tid == 0) sm.depth[0] = 0;
     dup = __syncthreads_or(dup);
     if (tid == 0 && dup) sm.status = TV_TREE_DUP_SIBLING;
-    for (int i = 1 + tid; i < n1; i += kNT) {
-      const int j = sm.parent[i], x = sm.token[i];
-      sm.gb[i] = Elem<T>::scalar(row_ptr<T>(P, P.target, b, j) + x);
-      sm.gs[i] = Elem<T>::scalar(row_ptr<T>(P, P.draft, b, j) + x);
+    // every node's parent logits at its token (the loads issued together)
+    float vb[kPer], vs[kPer];
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = 1 + tid + t * kNT;
+      vb[t] = vs[t] = 0.0f;
+      if (i < n1) {
+        const int j = sm.parent[i], x = sm.token[i];
+        vb[t] = Elem<T>::scalar(row_ptr<T>(P, P.target, b, j) + x);
+        vs[t] = Elem<T>::scalar(row_ptr<T>(P, P.draft, b, j) + x);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = 1 + tid + t * kNT;
+      if (i < n1) {
+        sm.gb[i] = vb[t];
+        sm.gs[i] = vs[t];
+      }
     }
     if (P.tmax) {
       // Row statistics given by the caller: every node with children has its
@@ -1283,17 +1349,34 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
   const int n1 = P.num_nodes;
   const size_t tree_off = static_cast<size_t>(b) * n1;
   const bool ok = sm.status == TV_TREE_OK;
-  // nodes below a chain of rate 0 that the traversal skipped
-  for (int i = 1 + tid; i < n1; i += kNT) {
-    if (sm.state[i] != TV_NODE_UNTESTED) continue;
-    for (int x = i; x > 0; x = sm.parent[x]) {
-      const int a = sm.parent[x];
-      if ((sm.flags[a] & kFlagPrunedBelow) && sm.rank[x] >= sm.prune_from[a]) {
-        sm.state[i] = TV_NODE_PRUNED;
-        sm.theta[i] = 0.0f;
-        break;
+  // nodes below a chain of rate 0 that the traversal skipped: an untested
+  // node is pruned if an edge on its path to the root leaves a node pruned
+  // below at or after its first pruned child (each thread's walks side by side)
+  constexpr int kPer = (kCap + kNT - 1) / kNT;
+  int x[kPer];
+#pragma unroll
+  for (int t = 0; t < kPer; ++t) {
+    const int i = 1 + tid + t * kNT;
+    x[t] = (i < n1 && sm.state[i] == TV_NODE_UNTESTED) ? i : 0;
+  }
+  for (;;) {
+    bool any = false;
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      if (x[t] > 0) {
+        const int a = sm.parent[x[t]];
+        if ((sm.flags[a] & kFlagPrunedBelow) && sm.rank[x[t]] >= sm.prune_from[a]) {
+          const int i = 1 + tid + t * kNT;
+          sm.state[i] = TV_NODE_PRUNED;
+          sm.theta[i] = 0.0f;
+          x[t] = 0;
+        } else {
+          x[t] = a;
+          any = any || a > 0;
+        }
       }
     }
+    if (!any) break;
   }
   __syncthreads();
   for (int i = tid; i < n1; i += kNT) {
@@ -1465,7 +1548,7 @@ __device__ __attribute__((always_inline)) bool combine(Lds<TreeSmem<kCap>>& sm,
 // the chunk sums finds the chunk, a wave scan over its units the unit, and the
 // lane holding that unit finds the token.
 constexpr int kSampleChunks = 256;      // chunk sums held at once (a window)
-constexpr int kSampleInFlight = 2;      // chunks per wave whose loads are in flight
+constexpr int kSampleInFlight = 4;      // chunks per wave whose loads are in flight
 
 template <typename T, class A, int kCap>
 __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch>& ws,
@@ -2119,7 +2202,7 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   __syncthreads();
   bool live = true;
   for (int b = g; b < P.batch; b += P.ngroups) {
-    begin_tree<T>(sm, Ps, ar, b);
+    begin_tree<T>(sm, ws, Ps, ar, b);
     for (;;) {
       controller_step<T, A>(sm, ws, Ps, ar, g, m, false);
       while (sm.cmd == kCmdLocalSample) {
