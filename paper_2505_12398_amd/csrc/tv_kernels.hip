@@ -713,7 +713,6 @@ template <int kCap>
 struct TreeSmem {
   // tree structure
   int16_t parent[kCap];
-  int16_t depth[kCap];
   int16_t child_start[kCap];
   int16_t child_list[kCap];
   int16_t next_child[kCap];        // children already removed (always a prefix)
@@ -745,6 +744,7 @@ struct TreeSmem {
   int has_tree, tree;
   int phase, cur, accepted, rejected, status;
   int rows_consulted, resid_passes, tests, pinit_next;
+  int any_pruned;                  // some node has kFlagPrunedBelow
   double alpha, beta;
   // command from the controller; a batch: pass 0 is the one the traversal
   // waits for, the others are STATS of nodes it will descend into
@@ -940,6 +940,7 @@ __device__ __forceinline__ void advance_impl(Lds<TreeSmem<kCap>>& sm, TraversalA
           // written when the tree finishes), and j itself is tested next
           sm.prune_from[j] = sm.next_child[j];
           sm.flags[j] |= kFlagPrunedBelow;
+          sm.any_pruned = 1;
           sm.next_child[j] = static_cast<int16_t>(sm.child_count[j]);
           ct.phase = kPhTest;
           continue;
@@ -1169,21 +1170,47 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, Ld
   const size_t tree_off = static_cast<size_t>(b) * n1;
   if (tid == 0) sm.status = TV_TREE_OK;
   __syncthreads();
+  // every load of the tree at once: links, tokens, uniforms, then each
+  // node's parent logits at its token (at clamped indices, so that they stay
+  // in the rows whatever the links; stored only once the tree is checked)
+  int pr[kPer], xr[kPer];
+  float ur[kPer], vb[kPer], vs[kPer];
+#pragma unroll
+  for (int t = 0; t < kPer; ++t) {
+    const int i = tid + t * kNT;
+    pr[t] = xr[t] = 0;
+    ur[t] = 0.0f;
+    if (i < n1) {
+      pr[t] = P.parents[tree_off + i];
+      xr[t] = P.tokens[tree_off + i];
+      ur[t] = P.uniforms[tree_off + i];
+    }
+  }
   int bad_parent = 0, bad_token = 0;
-  for (int i = tid; i < n1; i += kNT) {
-    const int p = P.parents[tree_off + i];
-    const int x = P.tokens[tree_off + i];
-    if (i == 0 ? p != -1 : (p < 0 || p >= i)) bad_parent = 1;
-    if (i > 0 && (x < 0 || x >= V)) bad_token = 1;
-    sm.parent[i] = static_cast<int16_t>(i == 0 ? -1 : (p < 0 || p >= i ? 0 : p));
-    sm.token[i] = x;
-    sm.u[i] = P.uniforms[tree_off + i];
-    sm.child_count[i] = 0;
-    sm.next_child[i] = 0;
-    sm.state[i] = TV_NODE_UNTESTED;
-    sm.flags[i] = 0;
-    sm.theta[i] = -1.0f;
-    sm.pini[i] = -1.0;
+#pragma unroll
+  for (int t = 0; t < kPer; ++t) {
+    const int i = tid + t * kNT;
+    vb[t] = vs[t] = 0.0f;
+    if (i < n1) {
+      const int p = pr[t], x = xr[t];
+      if (i == 0 ? p != -1 : (p < 0 || p >= i)) bad_parent = 1;
+      if (i > 0 && (x < 0 || x >= V)) bad_token = 1;
+      const int pc = (i == 0 || p < 0 || p >= i) ? 0 : p;
+      if (i > 0) {
+        const int xc = min(max(x, 0), V - 1);
+        vb[t] = Elem<T>::scalar(row_ptr<T>(P, P.target, b, pc) + xc);
+        vs[t] = Elem<T>::scalar(row_ptr<T>(P, P.draft, b, pc) + xc);
+      }
+      sm.parent[i] = static_cast<int16_t>(i == 0 ? -1 : pc);
+      sm.token[i] = x;
+      sm.u[i] = ur[t];
+      sm.child_count[i] = 0;
+      sm.next_child[i] = 0;
+      sm.state[i] = TV_NODE_UNTESTED;
+      sm.flags[i] = 0;
+      sm.theta[i] = -1.0f;
+      sm.pini[i] = -1.0;
+    }
   }
   bad_parent = __syncthreads_or(bad_parent);
   bad_token = __syncthreads_or(bad_token);
@@ -1238,64 +1265,29 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, Ld
         int r = 0;
         for (int k2 = 0; k2 < cnt; ++k2) {
           const int c = sm.child_list[s0 + k2];
+          const int xc = sm.token[c];
           r += c < i;
-          if (wo && c != i && sm.token[c] == x) dup = 1;
+          dup |= static_cast<int>(wo & (c != i) & (xc == x));
         }
         rk[t] = r;
       }
     }
     __syncthreads();
-    // in index order, and every node's depth (its walks to the root taken
-    // side by side)
-    int a[kPer], d[kPer];
+    // in index order
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
       const int i = 1 + tid + t * kNT;
-      a[t] = 0;
-      d[t] = 1;
       if (i < n1) {
-        const int p = sm.parent[i];
-        sm.child_list[sm.child_start[p] + rk[t]] = static_cast<int16_t>(i);
+        sm.child_list[sm.child_start[sm.parent[i]] + rk[t]] = static_cast<int16_t>(i);
         sm.rank[i] = static_cast<int16_t>(rk[t]);
-        a[t] = p;
       }
     }
-    for (;;) {
-      bool any = false;
-#pragma unroll
-      for (int t = 0; t < kPer; ++t) {
-        if (a[t] > 0) {
-          a[t] = sm.parent[a[t]];
-          ++d[t];
-          any = true;
-        }
-      }
-      if (!any) break;
-    }
-#pragma unroll
-    for (int t = 0; t < kPer; ++t) {
-      const int i = 1 + tid + t * kNT;
-      if (i < n1) sm.depth[i] = static_cast<int16_t>(d[t]);
-    }
-    if (tid == 0) sm.depth[0] = 0;
     dup = __syncthreads_or(dup);
     if (tid == 0 && dup) sm.status = TV_TREE_DUP_SIBLING;
-    // every node's parent logits at its token (the loads issued together)
-    float vb[kPer], vs[kPer];
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
-      const int i = 1 + tid + t * kNT;
-      vb[t] = vs[t] = 0.0f;
-      if (i < n1) {
-        const int j = sm.parent[i], x = sm.token[i];
-        vb[t] = Elem<T>::scalar(row_ptr<T>(P, P.target, b, j) + x);
-        vs[t] = Elem<T>::scalar(row_ptr<T>(P, P.draft, b, j) + x);
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < kPer; ++t) {
-      const int i = 1 + tid + t * kNT;
-      if (i < n1) {
+      const int i = tid + t * kNT;
+      if (i > 0 && i < n1) {
         sm.gb[i] = vb[t];
         sm.gs[i] = vs[t];
       }
@@ -1328,6 +1320,7 @@ __device__ __attribute__((noinline)) void begin_tree(Lds<TreeSmem<kCap>>& sm, Ld
     sm.accepted = -1;
     sm.rows_consulted = sm.resid_passes = sm.tests = 0;
     sm.pinit_next = 0;
+    sm.any_pruned = 0;
     init_node_state(sm, 0, 1.0);
     sm.res_y = -1;
     sm.cmd = kCmdNone;
@@ -1349,34 +1342,70 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
   const int n1 = P.num_nodes;
   const size_t tree_off = static_cast<size_t>(b) * n1;
   const bool ok = sm.status == TV_TREE_OK;
-  // nodes below a chain of rate 0 that the traversal skipped: an untested
-  // node is pruned if an edge on its path to the root leaves a node pruned
-  // below at or after its first pruned child (each thread's walks side by side)
-  constexpr int kPer = (kCap + kNT - 1) / kNT;
-  int x[kPer];
-#pragma unroll
-  for (int t = 0; t < kPer; ++t) {
-    const int i = 1 + tid + t * kNT;
-    x[t] = (i < n1 && sm.state[i] == TV_NODE_UNTESTED) ? i : 0;
-  }
-  for (;;) {
-    bool any = false;
+  // the accepted node's depth (thread 0 walks to the root meanwhile)
+  int depth = 0;
+  if (tid == 0 && ok)
+    for (int x = sm.accepted; x > 0; x = sm.parent[x]) ++depth;
+  // Nodes below a chain of rate 0 that the traversal skipped. The edge into
+  // node x is cut if x's parent is pruned below at or before x's rank; a node
+  // is pruned if an edge on its path to the root is cut. Pointer jumping:
+  // every node holds the OR of the cuts from itself up to (not including) its
+  // current ancestor, and each round doubles that span, so the rounds number
+  // log2 of the depth. prune_from and next_child, which the finished
+  // traversal no longer reads, hold the spans' cut flags and ancestors.
+  if (sm.any_pruned) {
+    constexpr int kPer = (kCap + kNT - 1) / kNT;
+    int anc[kPer], cut[kPer];
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
-      if (x[t] > 0) {
-        const int a = sm.parent[x[t]];
-        if ((sm.flags[a] & kFlagPrunedBelow) && sm.rank[x[t]] >= sm.prune_from[a]) {
-          const int i = 1 + tid + t * kNT;
-          sm.state[i] = TV_NODE_PRUNED;
-          sm.theta[i] = 0.0f;
-          x[t] = 0;
-        } else {
-          x[t] = a;
-          any = any || a > 0;
-        }
+      const int i = tid + t * kNT;
+      const bool in = i > 0 && i < n1;
+      const int p = in ? sm.parent[i] : 0;
+      // no short-circuit: a branch per condition would serialise the reads
+      const int f = sm.flags[p], ri = sm.rank[in ? i : 0], pf = sm.prune_from[p];
+      cut[t] = static_cast<int>(in & ((f & kFlagPrunedBelow) != 0) & (ri >= pf));
+      anc[t] = p;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = tid + t * kNT;
+      if (i < n1) {
+        sm.prune_from[i] = static_cast<int16_t>(cut[t]);
+        sm.next_child[i] = static_cast<int16_t>(anc[t]);
       }
     }
-    if (!any) break;
+    __syncthreads();
+    for (;;) {
+      int fa[kPer], aa[kPer];
+#pragma unroll
+      for (int t = 0; t < kPer; ++t) {
+        fa[t] = sm.prune_from[anc[t]];
+        aa[t] = sm.next_child[anc[t]];
+      }
+      __syncthreads();
+      int live = 0;
+#pragma unroll
+      for (int t = 0; t < kPer; ++t) {
+        const int i = tid + t * kNT;
+        cut[t] |= fa[t];
+        anc[t] = aa[t];
+        live |= anc[t];
+        if (i < n1) {
+          sm.prune_from[i] = static_cast<int16_t>(cut[t]);
+          sm.next_child[i] = static_cast<int16_t>(anc[t]);
+        }
+      }
+      if (!__syncthreads_or(live)) break;
+    }
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int i = tid + t * kNT;
+      if (cut[t] && i < n1 && sm.state[i] == TV_NODE_UNTESTED) {
+        sm.state[i] = TV_NODE_PRUNED;
+        sm.theta[i] = 0.0f;
+      }
+    }
   }
   __syncthreads();
   for (int i = tid; i < n1; i += kNT) {
@@ -1386,7 +1415,7 @@ __device__ __attribute__((always_inline)) void finish_tree(Lds<TreeSmem<kCap>>& 
   }
   if (tid == 0) {
     P.status[b] = sm.status;
-    P.accept_len[b] = ok ? sm.depth[sm.accepted] : -1;
+    P.accept_len[b] = ok ? depth : -1;
     P.accepted_node[b] = ok ? sm.accepted : -1;
     P.bonus_token[b] = ok ? sm.res_y : -1;
     if (P.counters) {
