@@ -1791,12 +1791,15 @@ __device__ __attribute__((noinline)) void local_sample(Lds<TreeSmem<kCap>>& sm, 
         }
         double C = incl - us;
         int y = -1, last = -1;
-        for (int e = 0; e < n; ++e) {
-          if (wd[e] > 0.0) {
-            last = tok0 + e;
-            if (!last_of_unit && y < 0 && tgt < C + wd[e]) y = tok0 + e;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {     // unrolled: wd stays in registers
+          if (e < n) {
+            if (wd[e] > 0.0) {
+              last = tok0 + e;
+              if (!last_of_unit && y < 0 && tgt < C + wd[e]) y = tok0 + e;
+            }
+            C += wd[e];
           }
-          C += wd[e];
         }
         sm.res_y = y >= 0 ? y : last;    // rounding inside the unit: its last positive weight
       }
