@@ -181,3 +181,24 @@ def test_peaked_rows(mode):
     u = torch.as_tensor(W.uniforms_np(rng, (B, n1)), device=DEV)
     check_sampler(torch.as_tensor(par, device=DEV), draft, 1.0, u, mode,
                   label=f"peaked mode={mode}")
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("V,dtype,B", [(151936, "bf16", 12), (100003, "f32", 12),
+                                       (1 << 20, "bf16", 4)])
+def test_chunks_of_several_blocks(V, dtype, B, mode):
+    """Vocabularies whose chunks span several 8-unit blocks, so that a chunk's
+    running maximum (and frame) rises inside the chunk: 16 units per chunk at
+    V = 151936 bf16 (the irregular N=60 workload's vocabulary) and V = 100003
+    fp32 (odd: misaligned rows), 64 units per chunk at the largest bf16
+    vocabulary, 2^20. Random 9-node trees, rows N(0, 2^2), every tree
+    compared."""
+    rng = np.random.default_rng(V % 1000 + 31 * mode)
+    n1 = 9
+    par = _random_trees(rng, B, n1, max_back=3)
+    z = torch.as_tensor(rng.normal(0.0, 2.0, (B, n1, V)).astype(np.float32), device=DEV)
+    draft = z.to(torch.bfloat16) if dtype == "bf16" else z
+    u = W.uniforms_np(rng, (B, n1))
+    check_sampler(torch.as_tensor(par, device=DEV), draft.contiguous(), 1.0,
+                  torch.as_tensor(u, device=DEV), mode, label=f"V={V} {dtype} mode={mode}")
+    del z, draft
+    torch.cuda.empty_cache()
