@@ -607,8 +607,11 @@ struct Round {
 // thread owns (vb + tid + i * kNT), in that order. Each step issues two rounds
 // of loads before any arithmetic and consumes the first round while the
 // second is still in flight. Loads past the stripe are clamped re-reads of its
-// last vector.
-template <typename T, bool TWO, int U, class F>
+// last vector. With kShort, a step whose stripe ends within its first round
+// issues no second round (whose loads would otherwise still be waited for):
+// the large-tree variant, whose stripes are short; the compact variant keeps
+// the loop as it is, where the branch measured slower.
+template <typename T, bool TWO, int U, bool kShort = false, class F>
 __device__ __forceinline__ void stream_stripe(const T* rb, const T* rs, int head,
                                               const SegRange& r, F&& f) {
   constexpr int kRound = kNT * U;
@@ -623,11 +626,12 @@ __device__ __forceinline__ void stream_stripe(const T* rb, const T* rs, int head
 #pragma unroll 1
   for (int base = r.vb; base < r.ve; base += 2 * kRound) {
     Round<T, TWO, U> x, y;
+    const bool second = !kShort || base + kRound < r.ve;
     x.load(rb, rs, head, base + tid, vmax);
-    y.load(rb, rs, head, base + kRound + tid, vmax);
+    if (second) y.load(rb, rs, head, base + kRound + tid, vmax);
     __builtin_amdgcn_sched_barrier(0);
     consume(x, base);
-    consume(y, base + kRound);
+    if (second) consume(y, base + kRound);
   }
 }
 
@@ -638,7 +642,7 @@ __device__ __forceinline__ void stream_stripe(const T* rb, const T* rs, int head
 // loads are in flight together; only the arithmetic is guarded.
 // ---------------------------------------------------------------------------
 
-template <typename T, class A, bool TWO>
+template <typename T, class A, bool TWO, bool kShort>
 __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
                              const SegRange& r, const A& ar, StripeResult& out) {
   constexpr int E = Elem<T>::E;
@@ -652,7 +656,7 @@ __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const
       online_add(os, xs, ar);
     }
   }
-  stream_stripe<T, TWO, kUnrollOf<A>>(rb, rs, g.head, r, [&](const uint4& vb, const uint4& vs) {
+  stream_stripe<T, TWO, kUnrollOf<A>, kShort>(rb, rs, g.head, r, [&](const uint4& vb, const uint4& vs) {
     float x[E];
     Elem<T>::unpack(vb, x);
     online_add(ob, x, ar);
@@ -684,7 +688,7 @@ __device__ void stripe_stats(Lds<WgScratch>& ws, const T* rb, const T* rs, const
   out.s1 = Ss;
 }
 
-template <typename T, class A, bool SD>
+template <typename T, class A, bool SD, bool kShort>
 __device__ void stripe_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const Geom& g,
                             const SegRange& r, const A& ar, const TermParams& p,
                             StripeResult& out) {
@@ -693,7 +697,7 @@ __device__ void stripe_wsum(Lds<WgScratch>& ws, const T* rb, const T* rs, const 
   const int tid = threadIdx.x;
   double acc = 0.0, sd = 0.0;
   if (r.first && tid < g.head) acc += scalar_weight<T, TM, true>(tm, rb, rs, tid, sd);
-  stream_stripe<T, true, kUnrollOf<A>>(rb, rs, g.head, r, [&](const uint4& vb, const uint4& vs) {
+  stream_stripe<T, true, kUnrollOf<A>, kShort>(rb, rs, g.head, r, [&](const uint4& vb, const uint4& vs) {
     acc += vec_sum<T, TM, true>(tm, vb, vs, sd);
   });
   if (r.last && tid < g.tail)
@@ -1911,17 +1915,17 @@ __device__ __forceinline__ void publish_done(const PP& P, int g, uint32_t seq) {
 }
 
 // One pass of a stripe (all threads): STATS, or SPASS / WSUM weights.
-template <typename T, class A>
+template <typename T, class A, bool kShort>
 __device__ __forceinline__ StripeResult stripe_pass(Lds<WgScratch>& ws, const T* rb, const T* rs,
                                                     const Geom& geo, const SegRange& r, int cmd,
                                                     const TermParams& tp, const A& ar) {
   StripeResult part;
   switch (cmd) {
-    case kCmdStats2: stripe_stats<T, A, true>(ws, rb, rs, geo, r, ar, part); break;
-    case kCmdStats1: stripe_stats<T, A, false>(ws, rb, rs, geo, r, ar, part); break;
+    case kCmdStats2: stripe_stats<T, A, true, kShort>(ws, rb, rs, geo, r, ar, part); break;
+    case kCmdStats1: stripe_stats<T, A, false, kShort>(ws, rb, rs, geo, r, ar, part); break;
     default:
-      if (cmd == kCmdSPassSd) stripe_wsum<T, A, true>(ws, rb, rs, geo, r, ar, tp, part);
-      else stripe_wsum<T, A, false>(ws, rb, rs, geo, r, ar, tp, part);
+      if (cmd == kCmdSPassSd) stripe_wsum<T, A, true, kShort>(ws, rb, rs, geo, r, ar, tp, part);
+      else stripe_wsum<T, A, false, kShort>(ws, rb, rs, geo, r, ar, tp, part);
       break;
   }
   return part;
@@ -2023,7 +2027,7 @@ __device__ __forceinline__ void await_desc(Lds<WgScratch>& ws, const Params& P, 
 
 // Contributor c of group g until the group has no tree left (all threads).
 // Returns false if the launch was abandoned.
-template <typename T, class A>
+template <typename T, class A, bool kShort>
 __device__ __forceinline__ bool help_group(Lds<WgScratch>& ws, const Params& P, const A& ar, int g,
                                            int c) {
   const int tid = threadIdx.x;
@@ -2043,7 +2047,7 @@ __device__ __forceinline__ bool help_group(Lds<WgScratch>& ws, const Params& P, 
         const T* rb = row_ptr<T>(P, P.target, tree, node);
         const T* rs = row_ptr<T>(P, P.draft, tree, node);
         const Geom geo = row_geom(rb, P.vocab);
-        const StripeResult part = stripe_pass<T, A>(ws, rb, rs, geo, stripe(geo, c, geff),
+        const StripeResult part = stripe_pass<T, A, kShort>(ws, rb, rs, geo, stripe(geo, c, geff),
                                                     ws.d_cmd[p], tp, ar);
         if (tid == 0) {
           ws.res[p].s0 = part.s0;
@@ -2062,7 +2066,7 @@ __device__ __forceinline__ bool help_group(Lds<WgScratch>& ws, const Params& P, 
 // the fewest helpers that still takes one, until none does. Workgroups that
 // look at the same time spread over the groups with that fewest count: each
 // starts its search at its own position.
-template <typename T, class A>
+template <typename T, class A, bool kShort>
 __device__ __forceinline__ void help_others(Lds<WgScratch>& ws, const Params& P, A ar,
                                             int g_self) {
   const int tid = threadIdx.x, lane = tid & 63;
@@ -2121,7 +2125,7 @@ __device__ __forceinline__ void help_others(Lds<WgScratch>& ws, const Params& P,
     __syncthreads();
     if (g2 < 0) return;                  // no group takes a helper
     if (h < 0) continue;
-    if (!help_group<T, A>(ws, P, ar, g2, P.G + h)) return;
+    if (!help_group<T, A, kShort>(ws, P, ar, g2, P.G + h)) return;
   }
 }
 
@@ -2150,8 +2154,8 @@ __device__ __forceinline__ void run_batch(Lds<TreeSmem<kCap>>& sm, Lds<WgScratch
     const T* rb = row_ptr<T>(P, P.target, b, node);
     const T* rs = row_ptr<T>(P, P.draft, b, node);
     const Geom geo = row_geom(rb, P.vocab);
-    const StripeResult part = stripe_pass<T, A>(ws, rb, rs, geo, stripe(geo, m, geff),
-                                                sm.bcmd[p], tp, ar);
+    const StripeResult part = stripe_pass<T, A, (kCap > kCapSmall)>(
+        ws, rb, rs, geo, stripe(geo, m, geff), sm.bcmd[p], tp, ar);
     if (tid == 0) {
       ws.res[p].s0 = part.s0;
       ws.res[p].s1 = part.s1;
@@ -2259,7 +2263,7 @@ __global__ void __launch_bounds__(kNT) verify_kernel(Params P, A ar) {
   // for their loads one by one rather than for all at once
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   // the group has no tree left: help the groups that still run
-  if (P.Gx > P.G) help_others<T, A>(ws, P, ar, g);
+  if (P.Gx > P.G) help_others<T, A, (kCap > kCapSmall)>(ws, P, ar, g);
 }
 
 // Vocabularies below this use the precise element path whatever the dtype:
