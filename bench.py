@@ -39,7 +39,7 @@ METRIC = ("verified trees/sec + achieved HBM GB/s (% peak), 64-node trees, V=128
 def kernel_hash() -> str:
     """Hash of every source the library is built from (the kernels, their
     launch code and the C-ABI) and of its header: a profile taken on other
-    sources no longer describes this build."""
+    sources no longer describes the library built from these."""
     h = hashlib.sha256()
     for path in sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)) + [HEADER]:
         h.update(os.path.basename(path).encode())
@@ -542,7 +542,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the verification of independent trees needs no "
-              "collectives, and only --gpus 1 is supported in this build.", file=sys.stderr)
+              "collectives, and only --gpus 1 is supported.", file=sys.stderr)
         sys.exit(2)
 
     import torch
