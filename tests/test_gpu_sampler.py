@@ -202,3 +202,19 @@ def test_chunks_of_several_blocks(V, dtype, B, mode):
                   torch.as_tensor(u, device=DEV), mode, label=f"V={V} {dtype} mode={mode}")
     del z, draft
     torch.cuda.empty_cache()
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("T,V,dtype", [(0.2, 128256, "bf16"), (2.0, 128256, "bf16"),
+                                       (0.2, 4099, "f32")])
+def test_temperatures(T, V, dtype, mode):
+    """The lowest temperature of the paper's sweep (Table 4), T = 0.2, where
+    k = log2(e)/T multiplies exponents by five and the integer frames take
+    large steps, and a high one, T = 2, on both element paths: the
+    benchmark's tree shapes and logit law, 16 trees, every tree compared."""
+    bt = W.make_batch(5, step=11, device=DEV, mode=mode, batch=16, vocab=V)
+    draft = bt["draft"].to(torch.bfloat16 if dtype == "bf16" else torch.float32).contiguous()
+    rng = np.random.default_rng(int(T * 10) + V + mode)
+    u = torch.as_tensor(W.uniforms_np(rng, tuple(bt["parents"].shape)), device=DEV)
+    check_sampler(bt["parents"], draft, T, u, mode, label=f"T={T} V={V} {dtype} mode={mode}")
+    del bt, draft
+    torch.cuda.empty_cache()
