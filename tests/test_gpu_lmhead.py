@@ -66,9 +66,12 @@ def _check_stats(got_bits, row_max, row_sum, T):
 
 
 @pytest.mark.parametrize("M,K,N,T", [(37, 72, 301, 1.0), (130, 200, 1000, 0.7),
-                                     (300, 4096, 2053, 1.9)])
+                                     (300, 4096, 2053, 1.9), (257, 512, 4097, 0.2),
+                                     (1, 8, 2, 1.0)])
 def test_lmhead_ragged_tiles(M, K, N, T):
-    """Row, column and K tails (none of M, N a multiple of 128, K of 64)."""
+    """Row, column and K tails (none of M, N a multiple of 128, K of 64), the
+    lowest temperature of the paper's sweep (T = 0.2, Table 4), and the
+    smallest shapes the library takes (one row, K = 8, V = 2)."""
     g = torch.Generator(device=DEV).manual_seed(M * 7 + N)
     x = torch.randn((M, K), generator=g, device=DEV).to(torch.bfloat16)
     w = (torch.randn((N, K), generator=g, device=DEV) * (3.0 / K ** 0.5)).to(torch.bfloat16)
